@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused tree-reduce + momentum-SGD step on one MI355X.
+
+One step = one fc_step launch over all K synthetic gradient replicas of a
+workload (reduce in binary-tree order, average, SGD with momentum and weight
+decay, write back w and v), with every input resident in device memory.
+
+Prints ONE JSON line: effective HBM GB/s of the step (algorithmic bytes per
+step / wall time per step over the timed steps), the kernel's roofline entry
+(algorithmic bytes / average kernel duration from HIP events, against the
+8 TB/s HBM3E peak), and the oracle timed on a bounded sample on one host
+core as a CPU baseline.
+
+    python bench.py [--workload googlenet] [--steps 200] [--warmup 20]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD published peak
+METRIC = "effective HBM GB/s (and % of peak) for tree-reduce+SGD step; µs per step"
+KERNEL_SRC = os.path.join(ROOT, "paper_1511_00175_amd", "csrc", "fc_kernels.hip")
+
+
+def kernel_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic(workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary for
+    this workload, or None when absent or taken on another kernel version."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def host_info():
+    model = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
+    """Time the oracle (one host core) on a contiguous window of the
+    workload's elements, all K replicas; returns the JSON object."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    segs = oracle.segments(wl.table())
+    ends = segs["offset"] + segs["length"]
+
+    def window(m):
+        # segments clipped to [0, m)
+        rows = []
+        for (o, n, lm, dm), e in zip(wl.table(), ends):
+            if o >= m:
+                break
+            rows.append((o, min(n, m - o), lm, dm))
+        return rows
+
+    def run(m):
+        rows = window(m)
+        r = reps[:, :m].cpu().numpy()
+        wh = w[:m].cpu().numpy()
+        vh = v[:m].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.step(rows, list(r), wh, vh, wl.lr, wl.mu, wl.wd, wl.batch, order=order)
+        dt = time.perf_counter() - t0
+        return dt, sum(n for _, n, _, _ in rows)
+
+    total = int(ends.max())
+    m = min(total, 1 << 16)
+    dt, n = run(m)
+    # grow the window to about target_s seconds of oracle work
+    m2 = min(total, int(m * target_s / max(dt, 1e-6)))
+    if m2 > m:
+        dt, n = run(m2)
+        m = m2
+    bytes_ = n * (wl.K * wl.s_g + 16)
+    model, ncpu = host_info()
+    return {"value": round(bytes_ / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} of {wl.n_params} parameters (elements [0, {m}) of the layout), all K={wl.K} "
+                      f"replicas, one fused step; {dt:.2f} s on 1 thread of {ncpu} ({model})",
+            "seconds": round(dt, 3), "us_per_step_equiv": round(dt / n * wl.n_params * 1e6, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="googlenet",
+                    choices=["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux", "alexnet_ungrouped"])
+    ap.add_argument("--order", default="tree", choices=["tree", "linear"])
+    ap.add_argument("--out", action="store_true", help="also write the raw sum")
+    ap.add_argument("--bcast", action="store_true", help="also broadcast w' to K worker copies")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--seed", type=int, default=1511)
+    ap.add_argument("--opts", default="", help="launch shape, e.g. block_threads=256,vecs_per_thread=1")
+    ap.add_argument("--profile-loop", type=int, default=0,
+                    help="after the measurement, launch this many extra steps (for rocprofv3 runs)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU only (the K workers are replicas on one device); "
+              "--gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1511_00175_amd as fc
+    from workloads import gen, tables
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    wl = tables.get(args.workload)
+    opts = {}
+    for kv in filter(None, args.opts.split(",")):
+        k, v = kv.split("=")
+        opts[k] = int(v)
+
+    print(f"# workload {wl.name}: K={wl.K} {wl.dtype} N={wl.n_params} segs={len(wl.segments)}", file=sys.stderr,
+          flush=True)
+    reps, w, v = gen.device_inputs(wl, args.seed, dev)
+    out = torch.zeros_like(w) if args.out else None
+    bcast = torch.zeros((wl.K, wl.padded), device=dev) if args.bcast else None
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, args.order, **opts)
+    info = plan.info()
+    torch.cuda.synchronize()
+
+    def step():
+        plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[2 * i].record(stream)
+        step()
+        ev[2 * i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    durs = [ev[2 * i].elapsed_time(ev[2 * i + 1]) * 1e-3 for i in range(args.steps)]
+    for _ in range(args.profile_loop):
+        step()
+    torch.cuda.synchronize()
+
+    bytes_step = wl.algorithmic_bytes(out=args.out, bcast=args.bcast)
+    ms_per_step = wall / args.steps * 1e3
+    value = bytes_step / (wall / args.steps) / 1e9
+    avg = sum(durs) / len(durs)
+    med = sorted(durs)[len(durs) // 2]
+    achieved = bytes_step / avg / 1e9
+    traffic = read_traffic(wl.name) if not (args.out or args.bcast or args.order != "tree" or opts) else None
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "us_per_step": round(ms_per_step * 1e3, 2),
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}_k{wl.K}_{wl.dtype}",
+            "K": wl.K, "n_params": wl.n_params, "segments": len(wl.segments), "replica_dtype": wl.dtype,
+            "order": args.order, "batch": wl.batch, "lr": wl.lr, "momentum": wl.mu, "weight_decay": wl.wd,
+            "write_sum": args.out, "broadcast": args.bcast,
+            "algorithmic_bytes_per_step": bytes_step,
+            "launch": {"grid": info.grid, "tiles": info.ntiles, "block_threads": info.block_threads,
+                       "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk,
+                       "nontemporal": info.nontemporal},
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "kernel": "fc::reduce_kernel (fused step)",
+            "kernel_us_avg": round(avg * 1e6, 2),
+            "kernel_us_median": round(med * 1e6, 2),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, reps, w, v, args.order, args.cpu_seconds)
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,176 @@
+/*
+ * fc.h -- C ABI of the MI355X (gfx950) gradient-aggregation + SGD library.
+ *
+ * The operations follow the problem statement of FireCaffe (Iandola et al.,
+ * arXiv 1511.00175):
+ *   - Sec. 6 "Implementing efficient data parallel training": every worker
+ *     computes the sum of weight gradients over its share of the batch, and
+ *     the workers' sums are added together;
+ *   - Sec. 6.2 "Reduction tree", Fig. 3b, Eq. 4: the element-wise sum is
+ *     formed in binary reduction-tree order (branching factor 2, depth
+ *     log2 p); Sec. 6.1 "Parameter server", Fig. 3a: the alternative adds all
+ *     workers' vectors one after another at one node;
+ *   - Fig. 3 caption and Sec. 6.1: the result is sent back to every worker,
+ *     which applies the update to its local copy of the model;
+ *   - Sec. 3 "Preliminaries", Sec. 7.1 item 2: batched SGD with momentum and
+ *     weight decay.
+ * On one GPU the K workers are K gradient replicas resident in device memory.
+ *
+ * Arithmetic (every operation one IEEE-754 binary32 op, round to nearest
+ * even, no contraction, subnormals kept):
+ *   s     = tree (or linear) sum over k of widen(grads[k][i])
+ *   ga    = s * c,             c    = 1.0f / (float)batch (host, once)
+ *   d     = ga + wd_j * w[i],  wd_j = wd * decay_mult_j
+ *   v'    = mu * v[i] + lr_j * d,  lr_j = lr * lr_mult_j
+ *   w'    = w[i] - v'
+ * Tree shape for any K: neighbours are paired level by level and an odd last
+ * node moves up unchanged (for K a power of two this is the balanced tree).
+ *
+ * Conventions for every entry point:
+ *   - All buffers are device pointers owned by the caller; the library never
+ *     frees or retains them beyond the call.  A plan owns only its own small
+ *     device tables (tile map, segment multipliers, replica pointer tables).
+ *   - Element i of a segment lives at element index i of every buffer (w, v,
+ *     out, g, src, each replica, each broadcast destination); elements that
+ *     belong to no segment are never written.
+ *   - Every pointer must be 16-byte aligned (FC_EALIGN otherwise).
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream) and never synchronize the host, except when a replica or
+ *     destination pointer table differs from the plan's previous call and
+ *     that call was on another stream (the library then waits for that
+ *     stream before replacing the table).  Calls on one plan must not run
+ *     concurrently from several host threads.
+ *   - Return value: FC_OK (0) or a negative error code (fc_strerror names
+ *     it).  Argument errors are detected before anything is enqueued.
+ */
+#ifndef FC_H
+#define FC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FC_OK 0
+#define FC_EINVAL (-1) /* bad argument: null pointer, K out of range, bad table, batch < 1 */
+#define FC_EALIGN (-2) /* pointer not 16-byte aligned, or a segment offset not a multiple of
+                          the replica vector width (4 elements fp32, 8 elements fp16) */
+#define FC_EALIAS (-3) /* a written buffer overlaps another buffer (see each call) */
+#define FC_EHIP (-4)   /* the HIP runtime reported an error (allocation, copy or launch) */
+#define FC_ENOMEM (-5) /* host allocation failed */
+
+/* One segment = one layer's weight or bias block (Sec. 3, Eq. 1).  Offsets and
+ * lengths are in elements.  Segments must be sorted by offset and must not
+ * overlap; lengths may be zero or any size; the multipliers scale lr and wd
+ * for this segment (1, 1 = uniform). */
+typedef struct {
+    uint64_t offset;
+    uint64_t length;
+    float lr_mult;
+    float decay_mult;
+} fc_segment;
+
+/* Storage type of the gradient replicas.  Accumulation, weights, velocity,
+ * the raw sum and broadcast copies are always fp32.  FC_F16 is the 16-bit
+ * gradient storage named in Sec. 8.2 "Reducing communication among servers";
+ * widening fp16 -> fp32 is exact. */
+typedef enum { FC_F32 = 0, FC_F16 = 1 } fc_dtype;
+
+/* Summation order: binary reduction tree (Sec. 6.2) or parameter-server
+ * linear order (Sec. 6.1). */
+typedef enum { FC_ORDER_TREE = 0, FC_ORDER_LINEAR = 1 } fc_order;
+
+typedef struct fc_plan fc_plan;
+
+/* Launch shape.  Results are bit-identical for every allowed setting; the
+ * fields only change speed.  Zero (or -1 for `nontemporal`) selects the
+ * default. */
+typedef struct {
+    int block_threads;   /* 64, 128 or 256 threads per block (default 256) */
+    int vecs_per_thread; /* 16-byte vectors per thread per replica: 1 or 2 (default 1) */
+    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 8) */
+    int nontemporal;     /* 1: replica loads carry the non-temporal hint; 0: plain loads */
+    int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
+} fc_launch_opts;
+
+/* Create a plan for K workers over a segment table (Sec. 6: one gradient
+ * vector per worker).  segs[0..nseg-1] is copied; nseg may be 0 (every call
+ * then does nothing).  1 <= K <= 1024.  Offsets must be multiples of 4
+ * elements (FC_F32) or 8 elements (FC_F16).  Allocates the plan's device
+ * tables on the current device with hipMalloc (FC_EHIP on failure).
+ * On success *plan receives the plan; on failure *plan is set to NULL. */
+int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,
+                   fc_order order);
+
+/* As fc_plan_create, with an explicit launch shape (NULL = defaults). */
+int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,
+                      fc_order order, const fc_launch_opts* opts);
+
+/* Free the plan and its device tables (NULL is ignored).  The caller must
+ * make sure no work that uses the plan is still running. */
+void fc_plan_destroy(fc_plan* plan);
+
+/* Reduce (Sec. 6.2, Fig. 3b; or Sec. 6.1 for FC_ORDER_LINEAR): for every
+ * segment element i, out[i] = sum over k of widen(grads[k][i]), unscaled.
+ *   grads : host array of K device pointers, replica k of the plan's dtype
+ *   out   : device fp32 buffer.  It may be exactly grads[k] for an FC_F32
+ *           plan (each element is read by the thread that writes it); any
+ *           other overlap with a replica is FC_EALIAS. */
+int fc_tree_reduce(fc_plan* plan, const void* const* grads, float* out, void* stream);
+
+/* One momentum-SGD step with weight decay from a raw sum g (Sec. 3, Sec. 7.1
+ * item 2; the averaging by 1/batch is the Sec. 6 equivalence with one GPU
+ * summing over the whole batch):
+ *   w, v : device fp32 weights and velocity, updated in place
+ *   g    : device fp32 raw tree sum (as written by fc_tree_reduce)
+ *   batch >= 1.  w, v and g must not overlap (FC_EALIAS). */
+int fc_sgd_step(fc_plan* plan, float* w, float* v, const float* g, float lr, float mu, float wd,
+                int batch, void* stream);
+
+/* Send one fp32 vector back down the tree (Fig. 3 caption): dst[k][i] =
+ * src[i] for every worker k < K and segment element i.
+ *   dst : host array of K device pointers.  No destination may overlap src
+ *         or another destination (FC_EALIAS). */
+int fc_broadcast(fc_plan* plan, const float* src, float* const* dst, void* stream);
+
+/* The whole step in one pass over memory: reduce, average, SGD, write back,
+ * and optionally keep the raw sum and broadcast w'.
+ *   grads     : host array of K device replica pointers (plan's dtype)
+ *   w, v      : device fp32 weights and velocity, updated in place
+ *   out       : NULL, or a device fp32 buffer that receives the raw sum (it
+ *               may be exactly grads[k] for an FC_F32 plan)
+ *   bcast_dst : NULL, or a host array of K device fp32 pointers that
+ *               receive w' (the workers' local model copies)
+ * Result bits equal fc_tree_reduce, then fc_sgd_step, then fc_broadcast of w.
+ * w, v, out and every destination must not overlap each other or a replica
+ * (FC_EALIAS), except out == grads[k] as above. */
+int fc_step(fc_plan* plan, const void* const* grads, float* w, float* v, float lr, float mu,
+            float wd, int batch, float* out, float* const* bcast_dst, void* stream);
+
+/* Static description of a message code (never NULL). */
+const char* fc_strerror(int code);
+
+/* Plan facts for benchmarking and tests. */
+typedef struct {
+    int K;
+    int nseg;
+    int dtype;           /* fc_dtype */
+    int order;           /* fc_order */
+    uint64_t n_elems;    /* sum of segment lengths */
+    uint64_t extent;     /* one past the last segment element */
+    int ntiles;          /* blocks of work in one launch */
+    int grid;            /* blocks launched */
+    int block_threads;
+    int vecs_per_thread;
+    int kchunk;
+    int nontemporal;
+} fc_plan_info;
+
+int fc_plan_query(const fc_plan* plan, fc_plan_info* info);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FC_H */

@@ -1,0 +1,97 @@
+"""MI355X (gfx950) gradient aggregation + momentum SGD, after FireCaffe
+(Iandola et al., arXiv 1511.00175): K workers' gradient replicas resident in
+device memory are summed in binary reduction-tree order (Sec. 6.2, Fig. 3b) or
+parameter-server order (Sec. 6.1, Fig. 3a), averaged over the batch, applied as
+momentum SGD with weight decay, and the updated weights are optionally sent
+back to every worker (Fig. 3 caption).
+
+The work is done by HIP kernels behind the C ABI of include/fc.h; this package
+only marshals torch tensors (device memory and the current stream) into it.
+"""
+from . import _fc
+from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FcError,  # noqa: F401
+                  fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query, fc_sgd_step, fc_step,
+                  fc_strerror, fc_tree_reduce)
+
+__all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_tree_reduce",
+           "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror"]
+
+_DTYPES = {"f32": FC_F32, "f16": FC_F16}
+_ORDERS = {"tree": FC_ORDER_TREE, "linear": FC_ORDER_LINEAR}
+
+
+def _stream(stream):
+    if stream is not None:
+        return int(stream) if not hasattr(stream, "cuda_stream") else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _rows(x):
+    """Device pointers of the K replicas: a list of tensors or the rows of a
+    2-D tensor (K, stride)."""
+    if isinstance(x, (list, tuple)):
+        return [t.data_ptr() for t in x]
+    if x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("replicas must be a list of tensors or a row-major 2-D tensor")
+    base, step = x.data_ptr(), x.stride(0) * x.element_size()
+    return [base + k * step for k in range(x.shape[0])]
+
+
+class Plan:
+    """One segment table and worker count (fc_plan).
+
+    segments: rows (offset, length[, lr_mult, decay_mult]) in elements.
+    dtype   : replica storage, "f32" or "f16".
+    order   : "tree" (reduction tree) or "linear" (parameter server).
+    opts    : launch shape (block_threads, vecs_per_thread, kchunk,
+              nontemporal, max_blocks); results do not depend on it.
+    """
+
+    def __init__(self, segments, K, dtype="f32", order="tree", **opts):
+        rc, h = fc_plan_create(segments, K, _DTYPES[dtype], _ORDERS[order], opts or None)
+        if rc:
+            raise FcError("fc_plan_create", rc)
+        self.handle = h
+        self.K = K
+        self.dtype = dtype
+        self.order = order
+
+    def close(self):
+        if self.handle:
+            fc_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self):
+        return fc_plan_query(self.handle)
+
+    def tree_reduce(self, grads, out, stream=None):
+        rc = fc_tree_reduce(self.handle, _rows(grads), _ptr(out), _stream(stream))
+        if rc:
+            raise FcError("fc_tree_reduce", rc)
+
+    def sgd_step(self, w, v, g, lr, mu, wd, batch, stream=None):
+        rc = fc_sgd_step(self.handle, _ptr(w), _ptr(v), _ptr(g), lr, mu, wd, batch, _stream(stream))
+        if rc:
+            raise FcError("fc_sgd_step", rc)
+
+    def broadcast(self, src, dst, stream=None):
+        rc = fc_broadcast(self.handle, _ptr(src), _rows(dst), _stream(stream))
+        if rc:
+            raise FcError("fc_broadcast", rc)
+
+    def step(self, grads, w, v, lr, mu, wd, batch, out=None, bcast=None, stream=None):
+        rc = fc_step(self.handle, _rows(grads), _ptr(w), _ptr(v), lr, mu, wd, batch, _ptr(out),
+                     None if bcast is None else _rows(bcast), _stream(stream))
+        if rc:
+            raise FcError("fc_step", rc)

@@ -1,0 +1,134 @@
+"""ctypes binding of libfc.so (include/fc.h), argument marshalling only.
+
+Every function here has the name of the C entry point it calls and passes
+its arguments through unchanged; all computation happens in the HIP kernels
+behind the C ABI.  If libfc.so is missing the import fails: there is no other
+implementation to fall back to.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("FC_LIBRARY", os.path.join(PKG, "libfc.so"))
+
+FC_OK, FC_EINVAL, FC_EALIGN, FC_EALIAS, FC_EHIP, FC_ENOMEM = 0, -1, -2, -3, -4, -5
+FC_F32, FC_F16 = 0, 1
+FC_ORDER_TREE, FC_ORDER_LINEAR = 0, 1
+
+
+class fc_segment(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_uint64), ("length", ctypes.c_uint64),
+                ("lr_mult", ctypes.c_float), ("decay_mult", ctypes.c_float)]
+
+
+class fc_launch_opts(ctypes.Structure):
+    _fields_ = [("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int), ("kchunk", ctypes.c_int),
+                ("nontemporal", ctypes.c_int), ("max_blocks", ctypes.c_int)]
+
+
+class fc_plan_info(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int), ("nseg", ctypes.c_int), ("dtype", ctypes.c_int), ("order", ctypes.c_int),
+                ("n_elems", ctypes.c_uint64), ("extent", ctypes.c_uint64), ("ntiles", ctypes.c_int),
+                ("grid", ctypes.c_int), ("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int),
+                ("kchunk", ctypes.c_int), ("nontemporal", ctypes.c_int)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
+                      "python paper_1511_00175_amd/build.py")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_vp = ctypes.c_void_p
+_pp = ctypes.POINTER(ctypes.c_void_p)
+_i, _f = ctypes.c_int, ctypes.c_float
+_plan_p = ctypes.c_void_p
+
+lib.fc_plan_create.argtypes = [ctypes.POINTER(_plan_p), ctypes.POINTER(fc_segment), _i, _i, _i, _i]
+lib.fc_plan_create_ex.argtypes = [ctypes.POINTER(_plan_p), ctypes.POINTER(fc_segment), _i, _i, _i, _i,
+                                  ctypes.POINTER(fc_launch_opts)]
+lib.fc_plan_destroy.argtypes = [_plan_p]
+lib.fc_plan_destroy.restype = None
+lib.fc_tree_reduce.argtypes = [_plan_p, _pp, _vp, _vp]
+lib.fc_sgd_step.argtypes = [_plan_p, _vp, _vp, _vp, _f, _f, _f, _i, _vp]
+lib.fc_broadcast.argtypes = [_plan_p, _vp, _pp, _vp]
+lib.fc_step.argtypes = [_plan_p, _pp, _vp, _vp, _f, _f, _f, _i, _vp, _pp, _vp]
+lib.fc_strerror.argtypes = [_i]
+lib.fc_strerror.restype = ctypes.c_char_p
+lib.fc_plan_query.argtypes = [_plan_p, ctypes.POINTER(fc_plan_info)]
+for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
+           "fc_plan_query"):
+    getattr(lib, _n).restype = ctypes.c_int
+
+
+class FcError(RuntimeError):
+    def __init__(self, fn, code):
+        self.code = code
+        super().__init__(f"{fn}: {fc_strerror(code)} ({code})")
+
+
+def _check(fn, rc):
+    if rc != FC_OK:
+        raise FcError(fn, rc)
+    return rc
+
+
+def _ptr_array(ptrs):
+    if ptrs is None:
+        return None
+    return (ctypes.c_void_p * len(ptrs))(*[int(p) for p in ptrs])
+
+
+def segment_array(rows):
+    """fc_segment[] from (offset, length[, lr_mult, decay_mult]) rows."""
+    rows = list(rows)
+    arr = (fc_segment * max(len(rows), 1))()
+    for i, r in enumerate(rows):
+        r = tuple(r)
+        arr[i] = fc_segment(int(r[0]), int(r[1]), float(r[2]) if len(r) > 2 else 1.0,
+                            float(r[3]) if len(r) > 3 else 1.0)
+    return arr, len(rows)
+
+
+def fc_strerror(code):
+    return lib.fc_strerror(int(code)).decode()
+
+
+def fc_plan_create(segs, K, gdt=FC_F32, order=FC_ORDER_TREE, opts=None):
+    """Returns (rc, plan handle).  `opts` is a dict of fc_launch_opts fields."""
+    arr, n = segment_array(segs)
+    h = _plan_p()
+    if opts is None:
+        rc = lib.fc_plan_create(ctypes.byref(h), arr, n, int(K), int(gdt), int(order))
+    else:
+        o = fc_launch_opts(0, 0, 0, -1, 0)
+        for k, v in opts.items():
+            setattr(o, k, int(v))
+        rc = lib.fc_plan_create_ex(ctypes.byref(h), arr, n, int(K), int(gdt), int(order), ctypes.byref(o))
+    return rc, h
+
+
+def fc_plan_destroy(plan):
+    lib.fc_plan_destroy(plan)
+
+
+def fc_plan_query(plan):
+    info = fc_plan_info()
+    _check("fc_plan_query", lib.fc_plan_query(plan, ctypes.byref(info)))
+    return info
+
+
+def fc_tree_reduce(plan, grads, out, stream=0):
+    return lib.fc_tree_reduce(plan, _ptr_array(grads), out, stream)
+
+
+def fc_sgd_step(plan, w, v, g, lr, mu, wd, batch, stream=0):
+    return lib.fc_sgd_step(plan, w, v, g, lr, mu, wd, int(batch), stream)
+
+
+def fc_broadcast(plan, src, dst, stream=0):
+    return lib.fc_broadcast(plan, src, _ptr_array(dst), stream)
+
+
+def fc_step(plan, grads, w, v, lr, mu, wd, batch, out=None, bcast_dst=None, stream=0):
+    return lib.fc_step(plan, _ptr_array(grads), w, v, lr, mu, wd, int(batch), out, _ptr_array(bcast_dst), stream)

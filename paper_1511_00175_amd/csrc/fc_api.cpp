@@ -1,0 +1,449 @@
+// Host side of the C ABI declared in include/fc.h: plan construction (tile
+// map, segment multipliers, replica pointer tables), argument validation and
+// kernel launch.  Every call validates before it enqueues anything.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "fc.h"
+#include "fc_internal.h"
+
+using fc::Tile;
+
+struct fc_plan {
+    int K = 0;
+    fc_dtype gdt = FC_F32;
+    fc_order order = FC_ORDER_TREE;
+    int vec = 4;        // elements per 16-byte replica vector
+    int sg = 4;         // bytes per replica element
+    std::vector<fc_segment> segs;
+    uint64_t n_elems = 0;
+    uint64_t extent = 0;  // one past the last segment element
+    fc::Shape shape{};
+    int ntiles = 0;
+    int grid = 0;
+    int device = 0;
+
+    Tile* d_tiles = nullptr;
+    float* d_mults = nullptr;
+    const void** d_grads = nullptr;  // K replica pointers
+    float** d_dst = nullptr;         // K broadcast pointers
+
+    // host copies of what the device pointer tables hold (valid flags)
+    std::vector<const void*> h_grads;
+    std::vector<float*> h_dst;
+    bool grads_valid = false;
+    bool dst_valid = false;
+    hipStream_t last_stream = nullptr;
+    bool have_last_stream = false;
+};
+
+namespace {
+
+constexpr int K_MAX = 1024;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Span {
+    uintptr_t lo, hi;  // [lo, hi)
+    bool written;
+    int id;            // distinct buffer id; replicas share role 0 and differ by id
+    bool replica;
+};
+
+bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Written buffers may not overlap any other buffer, except that `out` may be
+// exactly a replica of an FC_F32 plan (each element is read by the thread
+// that writes it).  Read-only buffers may overlap each other.
+int check_aliasing(const std::vector<Span>& spans, int out_id, bool f32) {
+    const size_t n = spans.size();
+    for (size_t i = 0; i < n; ++i) {
+        const Span& a = spans[i];
+        if (a.hi == a.lo) continue;
+        for (size_t j = i + 1; j < n; ++j) {
+            const Span& b = spans[j];
+            if (b.hi == b.lo) continue;
+            if (!a.written && !b.written) continue;
+            if (!overlap(a, b)) continue;
+            const bool exact_out_alias =
+                f32 && ((a.id == out_id && b.replica) || (b.id == out_id && a.replica)) && a.lo == b.lo &&
+                a.hi == b.hi;
+            if (!exact_out_alias) return FC_EALIAS;
+        }
+    }
+    return FC_OK;
+}
+
+int hip_rc(hipError_t e) { return e == hipSuccess ? FC_OK : FC_EHIP; }
+
+// Replace a device pointer table if its contents differ from the last call.
+// The copy is ordered on `s`; if the previous call ran on another stream,
+// that stream is drained first so that no running kernel still reads the
+// table being replaced.
+template <typename P>
+int update_table(fc_plan* p, std::vector<P>& host, bool& valid, P* dev, const P* want, hipStream_t s) {
+    const size_t K = static_cast<size_t>(p->K);
+    if (valid && std::equal(host.begin(), host.end(), want)) return FC_OK;
+    if (p->have_last_stream && p->last_stream != s) {
+        if (hipStreamSynchronize(p->last_stream) != hipSuccess) return FC_EHIP;
+    }
+    host.assign(want, want + K);
+    valid = false;
+    if (hipMemcpyAsync(dev, host.data(), K * sizeof(P), hipMemcpyHostToDevice, s) != hipSuccess)
+        return FC_EHIP;
+    valid = true;
+    return FC_OK;
+}
+
+void note_stream(fc_plan* p, hipStream_t s) {
+    p->last_stream = s;
+    p->have_last_stream = true;
+}
+
+int validate_opts(const fc_launch_opts* o, fc::Shape& sh) {
+    sh.block = 256;
+    sh.vecs = 1;
+    sh.kchunk = 8;
+    sh.nontemporal = 0;
+    if (!o) return FC_OK;
+    if (o->block_threads) {
+        if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
+        sh.block = o->block_threads;
+    }
+    if (o->vecs_per_thread) {
+        if (o->vecs_per_thread != 1 && o->vecs_per_thread != 2) return FC_EINVAL;
+        sh.vecs = o->vecs_per_thread;
+    }
+    if (o->kchunk) {
+        if (o->kchunk != 8 && o->kchunk != 16) return FC_EINVAL;
+        sh.kchunk = o->kchunk;
+    }
+    if (o->nontemporal != -1) {
+        if (o->nontemporal != 0 && o->nontemporal != 1) return FC_EINVAL;
+        sh.nontemporal = o->nontemporal;
+    }
+    if (o->max_blocks < 0) return FC_EINVAL;
+    return FC_OK;
+}
+
+int bit_length(int x) {
+    int n = 0;
+    while (x > 0) {
+        ++n;
+        x >>= 1;
+    }
+    return n;
+}
+
+void free_plan(fc_plan* p) {
+    if (!p) return;
+    if (p->d_tiles) (void)hipFree(p->d_tiles);
+    if (p->d_mults) (void)hipFree(p->d_mults);
+    if (p->d_grads) (void)hipFree(p->d_grads);
+    if (p->d_dst) (void)hipFree(p->d_dst);
+    delete p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fc_strerror(int code) {
+    switch (code) {
+        case FC_OK: return "success";
+        case FC_EINVAL: return "invalid argument";
+        case FC_EALIGN: return "misaligned pointer or segment offset";
+        case FC_EALIAS: return "a written buffer overlaps another buffer";
+        case FC_EHIP: return "HIP runtime error";
+        case FC_ENOMEM: return "out of host memory";
+        default: return "unknown error code";
+    }
+}
+
+int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt, fc_order order,
+                      const fc_launch_opts* opts) {
+    if (!plan) return FC_EINVAL;
+    *plan = nullptr;
+    if (nseg < 0 || (nseg > 0 && !segs)) return FC_EINVAL;
+    if (K < 1 || K > K_MAX) return FC_EINVAL;
+    if (gdt != FC_F32 && gdt != FC_F16) return FC_EINVAL;
+    if (order != FC_ORDER_TREE && order != FC_ORDER_LINEAR) return FC_EINVAL;
+    fc::Shape sh{};
+    int rc = validate_opts(opts, sh);
+    if (rc) return rc;
+
+    const int vec = gdt == FC_F16 ? 8 : 4;
+    uint64_t end = 0, n_elems = 0;
+    for (int j = 0; j < nseg; ++j) {
+        const fc_segment& s = segs[j];
+        if (s.offset % static_cast<uint64_t>(vec)) return FC_EALIGN;
+        if (s.length > UINT64_MAX - s.offset) return FC_EINVAL;
+        if (j > 0 && s.offset < end) return FC_EINVAL;  // unsorted or overlapping
+        end = std::max(end, s.offset + s.length);
+        n_elems += s.length;
+    }
+    // byte offsets of every element must fit in 64 bits for every buffer
+    if (end > (UINT64_MAX / 8)) return FC_EINVAL;
+
+    fc_plan* p = new (std::nothrow) fc_plan();
+    if (!p) return FC_ENOMEM;
+    p->K = K;
+    p->gdt = gdt;
+    p->order = order;
+    p->vec = vec;
+    p->sg = gdt == FC_F16 ? 2 : 4;
+    p->n_elems = n_elems;
+    p->extent = end;
+    sh.dtype = gdt;
+    sh.tree = order == FC_ORDER_TREE;
+    const int need = bit_length(K / sh.kchunk);
+    if (need > fc::MAXD_LARGE) {
+        delete p;
+        return FC_EINVAL;
+    }
+    sh.maxd = need <= fc::MAXD_SMALL ? fc::MAXD_SMALL : fc::MAXD_LARGE;
+    p->shape = sh;
+
+    // Tile map: each segment is cut into tiles of at most block*vecs vectors;
+    // a length that is not a multiple of the vector width leaves a tail tile.
+    std::vector<Tile> tiles;
+    std::vector<float> mults;
+    try {
+        p->segs.assign(segs, segs + nseg);
+        mults.resize(2 * static_cast<size_t>(std::max(nseg, 1)));
+        const uint64_t tile_vecs = static_cast<uint64_t>(sh.block) * sh.vecs;
+        for (int j = 0; j < nseg; ++j) {
+            const fc_segment& s = segs[j];
+            mults[2 * j] = s.lr_mult;
+            mults[2 * j + 1] = s.decay_mult;
+            const uint64_t nvec = s.length / vec;
+            const uint64_t tail = s.length % vec;
+            for (uint64_t v0 = 0; v0 < nvec; v0 += tile_vecs) {
+                Tile t;
+                t.start = s.offset + v0 * vec;
+                t.count = static_cast<uint32_t>(std::min(tile_vecs, nvec - v0));
+                t.seg = static_cast<uint32_t>(j);
+                tiles.push_back(t);
+            }
+            if (tail) {
+                Tile t;
+                t.start = s.offset + nvec * vec;
+                t.count = static_cast<uint32_t>(tail);
+                t.seg = static_cast<uint32_t>(j) | fc::TAIL_BIT;
+                tiles.push_back(t);
+            }
+        }
+        p->h_grads.assign(K, nullptr);
+        p->h_dst.assign(K, nullptr);
+    } catch (const std::bad_alloc&) {
+        delete p;
+        return FC_ENOMEM;
+    }
+    if (tiles.size() > static_cast<size_t>(INT32_MAX)) {
+        delete p;
+        return FC_EINVAL;
+    }
+    p->ntiles = static_cast<int>(tiles.size());
+    int grid = p->ntiles;
+    if (opts && opts->max_blocks > 0) grid = std::min(grid, opts->max_blocks);
+    p->grid = grid;
+
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return FC_EHIP;
+    }
+    bool ok = hipMalloc(&p->d_tiles, std::max<size_t>(tiles.size(), 1) * sizeof(Tile)) == hipSuccess &&
+              hipMalloc(&p->d_mults, mults.size() * sizeof(float)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&p->d_grads), K * sizeof(void*)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&p->d_dst), K * sizeof(float*)) == hipSuccess;
+    if (ok && !tiles.empty())
+        ok = hipMemcpy(p->d_tiles, tiles.data(), tiles.size() * sizeof(Tile), hipMemcpyHostToDevice) == hipSuccess;
+    if (ok)
+        ok = hipMemcpy(p->d_mults, mults.data(), mults.size() * sizeof(float), hipMemcpyHostToDevice) ==
+             hipSuccess;
+    if (!ok) {
+        free_plan(p);
+        return FC_EHIP;
+    }
+    *plan = p;
+    return FC_OK;
+}
+
+int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt, fc_order order) {
+    return fc_plan_create_ex(plan, segs, nseg, K, gdt, order, nullptr);
+}
+
+void fc_plan_destroy(fc_plan* plan) { free_plan(plan); }
+
+int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
+    if (!p || !info) return FC_EINVAL;
+    info->K = p->K;
+    info->nseg = static_cast<int>(p->segs.size());
+    info->dtype = p->gdt;
+    info->order = p->order;
+    info->n_elems = p->n_elems;
+    info->extent = p->extent;
+    info->ntiles = p->ntiles;
+    info->grid = p->grid;
+    info->block_threads = p->shape.block;
+    info->vecs_per_thread = p->shape.vecs;
+    info->kchunk = p->shape.kchunk;
+    info->nontemporal = p->shape.nontemporal;
+    return FC_OK;
+}
+
+namespace {
+
+// Byte extent of a buffer of `elem` bytes per element covering the plan.
+Span span_of(const fc_plan* p, const void* ptr, int elem, bool written, int id, bool replica) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+    return Span{lo, lo + static_cast<uintptr_t>(p->extent) * elem, written, id, replica};
+}
+
+enum { ID_W = 1, ID_V, ID_OUT, ID_G, ID_SRC, ID_REPLICA0 = 16 };
+
+int check_replicas(const fc_plan* p, const void* const* grads, std::vector<Span>& spans) {
+    if (!grads) return FC_EINVAL;
+    for (int k = 0; k < p->K; ++k) {
+        if (!grads[k]) return FC_EINVAL;
+        if (!aligned16(grads[k])) return FC_EALIGN;
+        spans.push_back(span_of(p, grads[k], p->sg, false, ID_REPLICA0 + k, true));
+    }
+    return FC_OK;
+}
+
+int check_dsts(const fc_plan* p, float* const* dst, std::vector<Span>& spans) {
+    for (int k = 0; k < p->K; ++k) {
+        if (!dst[k]) return FC_EINVAL;
+        if (!aligned16(dst[k])) return FC_EALIGN;
+        spans.push_back(span_of(p, dst[k], 4, true, ID_REPLICA0 + p->K + k, false));
+    }
+    return FC_OK;
+}
+
+}  // namespace
+
+int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* stream) {
+    if (!p || !out) return FC_EINVAL;
+    if (!aligned16(out)) return FC_EALIGN;
+    std::vector<Span> spans;
+    int rc = check_replicas(p, grads, spans);
+    if (rc) return rc;
+    spans.push_back(span_of(p, out, 4, true, ID_OUT, false));
+    rc = check_aliasing(spans, ID_OUT, p->gdt == FC_F32);
+    if (rc) return rc;
+    if (p->ntiles == 0) return FC_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    if (rc) return rc;
+    fc::ReduceArgs a{};
+    a.tiles = p->d_tiles;
+    a.ntiles = p->ntiles;
+    a.mults = p->d_mults;
+    a.grads = p->d_grads;
+    a.K = p->K;
+    a.out = out;
+    rc = hip_rc(fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s));
+    note_stream(p, s);
+    return rc;
+}
+
+int fc_sgd_step(fc_plan* p, float* w, float* v, const float* g, float lr, float mu, float wd, int batch,
+                void* stream) {
+    if (!p || !w || !v || !g || batch < 1) return FC_EINVAL;
+    if (!aligned16(w) || !aligned16(v) || !aligned16(g)) return FC_EALIGN;
+    std::vector<Span> spans = {span_of(p, w, 4, true, ID_W, false), span_of(p, v, 4, true, ID_V, false),
+                               span_of(p, g, 4, false, ID_G, false)};
+    int rc = check_aliasing(spans, -1, false);
+    if (rc) return rc;
+    if (p->ntiles == 0) return FC_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    fc::SgdArgs a{};
+    a.tiles = p->d_tiles;
+    a.ntiles = p->ntiles;
+    a.mults = p->d_mults;
+    a.w = w;
+    a.v = v;
+    a.g = g;
+    a.lr = lr;
+    a.mu = mu;
+    a.wd = wd;
+    a.c = 1.0f / static_cast<float>(batch);
+    rc = hip_rc(fc::launch_sgd(p->shape, p->grid, a, s));
+    note_stream(p, s);
+    return rc;
+}
+
+int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) {
+    if (!p || !src || !dst) return FC_EINVAL;
+    if (!aligned16(src)) return FC_EALIGN;
+    std::vector<Span> spans = {span_of(p, src, 4, false, ID_SRC, false)};
+    int rc = check_dsts(p, dst, spans);
+    if (rc) return rc;
+    rc = check_aliasing(spans, -1, false);
+    if (rc) return rc;
+    if (p->ntiles == 0) return FC_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, dst, s);
+    if (rc) return rc;
+    fc::BcastArgs a{};
+    a.tiles = p->d_tiles;
+    a.ntiles = p->ntiles;
+    a.src = src;
+    a.dst = p->d_dst;
+    a.K = p->K;
+    rc = hip_rc(fc::launch_bcast(p->shape, p->grid, a, s));
+    note_stream(p, s);
+    return rc;
+}
+
+int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
+            float* out, float* const* bcast_dst, void* stream) {
+    if (!p || !w || !v || batch < 1) return FC_EINVAL;
+    if (!aligned16(w) || !aligned16(v) || (out && !aligned16(out))) return FC_EALIGN;
+    std::vector<Span> spans;
+    int rc = check_replicas(p, grads, spans);
+    if (rc) return rc;
+    spans.push_back(span_of(p, w, 4, true, ID_W, false));
+    spans.push_back(span_of(p, v, 4, true, ID_V, false));
+    if (out) spans.push_back(span_of(p, out, 4, true, ID_OUT, false));
+    if (bcast_dst) {
+        rc = check_dsts(p, bcast_dst, spans);
+        if (rc) return rc;
+    }
+    rc = check_aliasing(spans, out ? ID_OUT : -1, p->gdt == FC_F32);
+    if (rc) return rc;
+    if (p->ntiles == 0) return FC_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    if (rc) return rc;
+    if (bcast_dst) {
+        rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, bcast_dst, s);
+        if (rc) return rc;
+    }
+    fc::ReduceArgs a{};
+    a.tiles = p->d_tiles;
+    a.ntiles = p->ntiles;
+    a.mults = p->d_mults;
+    a.grads = p->d_grads;
+    a.K = p->K;
+    a.w = w;
+    a.v = v;
+    a.out = out;
+    a.dst = bcast_dst ? p->d_dst : nullptr;
+    a.lr = lr;
+    a.mu = mu;
+    a.wd = wd;
+    a.c = 1.0f / static_cast<float>(batch);
+    rc = hip_rc(fc::launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s));
+    note_stream(p, s);
+    return rc;
+}
+
+}  // extern "C"

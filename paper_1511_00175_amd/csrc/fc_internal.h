@@ -1,0 +1,78 @@
+// Internal interface between the host library (fc_api.cpp) and the kernels
+// (fc_kernels.hip).  Not installed; the public ABI is include/fc.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fc {
+
+// One block's unit of work.  A vector tile covers `count` 16-byte replica
+// vectors (count <= block_threads * vecs_per_thread) starting at element
+// `start`, all inside segment `seg & SEG_MASK`.  A tail tile (bit TAIL_BIT of
+// `seg` set) covers the last `count` < vector-width elements of a segment
+// whose length is not a multiple of the vector width; its lanes work on one
+// element each.
+struct Tile {
+    uint64_t start;
+    uint32_t count;
+    uint32_t seg;
+};
+static_assert(sizeof(Tile) == 16, "Tile is loaded as one 16-byte scalar load");
+
+constexpr uint32_t TAIL_BIT = 0x80000000u;
+constexpr uint32_t SEG_MASK = 0x7fffffffu;
+
+enum Mode { MODE_REDUCE = 0, MODE_STEP = 1 };
+
+struct Shape {
+    int dtype;        // fc_dtype
+    int tree;         // 1 tree order, 0 linear
+    int block;        // threads per block
+    int vecs;         // 16-byte vectors per thread per replica (1 or 2)
+    int kchunk;       // replicas loaded per batch (8 or 16)
+    int nontemporal;  // non-temporal replica loads
+    int maxd;         // depth of the pending-subtree stack (>= bit length of K / kchunk)
+};
+
+struct ReduceArgs {
+    const Tile* tiles;
+    int ntiles;
+    const float* mults;           // per segment j: lr_mult at 2j, decay_mult at 2j+1
+    const void* const* grads;     // device table of K replica pointers
+    int K;
+    float* w;
+    float* v;
+    float* out;                   // raw sum or nullptr
+    float* const* dst;            // device table of K broadcast pointers, or nullptr
+    float lr, mu, wd, c;          // c = 1.0f / (float)batch
+};
+
+struct SgdArgs {
+    const Tile* tiles;
+    int ntiles;
+    const float* mults;
+    float* w;
+    float* v;
+    const float* g;
+    float lr, mu, wd, c;
+};
+
+struct BcastArgs {
+    const Tile* tiles;
+    int ntiles;
+    const float* src;
+    float* const* dst;
+    int K;
+};
+
+// Largest pending-subtree stack depth compiled; plans whose K / kchunk needs
+// more are rejected at creation.
+constexpr int MAXD_SMALL = 5;
+constexpr int MAXD_LARGE = 9;
+
+hipError_t launch_reduce(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
+hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s);
+hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s);
+
+}  // namespace fc

@@ -1,0 +1,525 @@
+// Kernels of the gradient-aggregation + SGD step for gfx950 (CDNA4).
+//
+// The work is a bandwidth-bound reduction: every element of every replica is
+// read once, the K values of one parameter are added in registers, and the
+// parameter's weight and velocity are updated in the same pass.  Arithmetic
+// intensity is at most (K + 6) flops per (4K + 16) bytes, far below the ridge
+// point of the vector units, so there are no matrix-core instructions here;
+// the design goals are full 16-byte coalesced loads, many loads in flight per
+// thread, and a summation order that is fixed by construction.
+//
+// Summation order (Sec. 6.2 "Reduction tree", Fig. 3b): leaves are replicas
+// 0..K-1 in order; neighbours are paired level by level and an odd last node
+// moves up unchanged.  The same tree is produced by a binary counter over
+// leaves: push each leaf (or each balanced subtree of kchunk consecutive
+// leaves) and, while the two newest pending subtrees have equal size, replace
+// them by (older + newer); at the end add the pending subtrees from the
+// newest to the oldest, each older one on the left.  Pending subtrees live in
+// a register stack indexed by the bit position of the counter, so every index
+// is a compile-time constant after unrolling.
+//
+// Parameter-server order (Sec. 6.1, Fig. 3a): ((x0 + x1) + x2) + ...
+//
+// Update (Sec. 3, Sec. 7.1 item 2, Caffe convention):
+//   ga = s*c ; d = ga + wd_j*w ; v' = mu*v + lr_j*d ; w' = w - v'
+// Every operation is one rounded fp32 op: contraction is disabled below and
+// the library is built with -ffp-contract=off.
+#include <type_traits>
+
+#include "fc.h"
+#include "fc_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace fc {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+template <int N> constexpr int ilog2() { return N <= 1 ? 0 : 1 + ilog2<N / 2>(); }
+
+// Address spaces.  Plan tables (tiles, segment multipliers, pointer tables)
+// are never written while a kernel runs: reading them through the constant
+// address space lets the compiler use scalar loads.  Buffers are device
+// (global) memory: replica pointers read from a table are cast to the global
+// address space so that loads take the form  global_load v, v_off32, s_base.
+#define FC_CONST __attribute__((address_space(4)))
+#define FC_GLOBAL __attribute__((address_space(1)))
+
+typedef const FC_GLOBAL char* gptr_t;
+typedef FC_GLOBAL char* gptr_w_t;
+
+// scalar (pointer or number) element i of a plan table
+template <typename T> __device__ __forceinline__ T ldc(const T* p, int i) {
+    return ((const FC_CONST T*)p)[i];
+}
+
+__device__ __forceinline__ Tile ld_tile(const Tile* tiles, int t) {
+    typedef unsigned int u4_t __attribute__((ext_vector_type(4)));
+    const u4_t x = ((const FC_CONST u4_t*)tiles)[t];
+    Tile r;
+    r.start = static_cast<uint64_t>(x.x) | (static_cast<uint64_t>(x.y) << 32);
+    r.count = x.z;
+    r.seg = x.w;
+    return r;
+}
+
+__device__ __forceinline__ gptr_t gread(const void* p) { return (gptr_t)p; }
+__device__ __forceinline__ gptr_w_t gwrite(void* p) { return (gptr_w_t)p; }
+
+// ------------------------------------------------------------------ replica loads
+// Rep<DT, V>: V consecutive replica elements starting at element e.
+template <int DT, int V> struct Rep;
+
+// load(base, off): `base` is the replica's address of the tile's first
+// element (uniform), `off` the lane's byte offset inside the tile.
+template <> struct Rep<FC_F32, 4> {
+    typedef f4 raw;
+    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        const FC_GLOBAL f4* q = reinterpret_cast<const FC_GLOBAL f4*>(base + off);
+        if constexpr (NT) return __builtin_nontemporal_load(q);
+        else return *q;
+    }
+    __device__ static __forceinline__ void widen(const raw& r, float* x) {
+        x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
+    }
+};
+
+template <> struct Rep<FC_F32, 1> {
+    typedef float raw;
+    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        const FC_GLOBAL float* q = reinterpret_cast<const FC_GLOBAL float*>(base + off);
+        if constexpr (NT) return __builtin_nontemporal_load(q);
+        else return *q;
+    }
+    __device__ static __forceinline__ void widen(const raw& r, float* x) { x[0] = r; }
+};
+
+// fp16 storage: binary16 -> binary32 is exact for every pattern.
+template <> struct Rep<FC_F16, 8> {
+    typedef u4 raw;
+    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        const FC_GLOBAL u4* q = reinterpret_cast<const FC_GLOBAL u4*>(base + off);
+        if constexpr (NT) return __builtin_nontemporal_load(q);
+        else return *q;
+    }
+    __device__ static __forceinline__ void widen(const raw& r, float* x) {
+        const h8 h = __builtin_bit_cast(h8, r);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = static_cast<float>(h[i]);
+    }
+};
+
+template <> struct Rep<FC_F16, 1> {
+    typedef unsigned short raw;
+    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        const FC_GLOBAL unsigned short* q = reinterpret_cast<const FC_GLOBAL unsigned short*>(base + off);
+        if constexpr (NT) return __builtin_nontemporal_load(q);
+        else return *q;
+    }
+    __device__ static __forceinline__ void widen(const raw& r, float* x) {
+        x[0] = static_cast<float>(__builtin_bit_cast(_Float16, r));
+    }
+};
+
+// ------------------------------------------------------------------ fp32 vectors
+// V consecutive fp32 values at byte offset `off` from the uniform base.
+template <int V> __device__ __forceinline__ void ld32(gptr_t base, uint32_t off, float* x) {
+    if constexpr (V == 1) {
+        x[0] = *reinterpret_cast<const FC_GLOBAL float*>(base + off);
+    } else {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            const f4 t = *reinterpret_cast<const FC_GLOBAL f4*>(base + off + 16 * q);
+            x[4 * q + 0] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
+        }
+    }
+}
+
+template <int V> __device__ __forceinline__ void st32(gptr_w_t base, uint32_t off, const float* x) {
+    if constexpr (V == 1) {
+        *reinterpret_cast<FC_GLOBAL float*>(base + off) = x[0];
+    } else {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            f4 t;
+            t.x = x[4 * q + 0]; t.y = x[4 * q + 1]; t.z = x[4 * q + 2]; t.w = x[4 * q + 3];
+            *reinterpret_cast<FC_GLOBAL f4*>(base + off + 16 * q) = t;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ accumulators
+// Partial sums are plain float[U][V] arrays, copied and added element by
+// element with constant indices so that they stay in registers.
+template <int U, int V> struct Acc {
+    float a[U][V];
+};
+
+template <int U, int V> __device__ __forceinline__ void set(Acc<U, V>& d, const Acc<U, V>& x) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < V; ++i) d.a[u][i] = x.a[u][i];
+}
+
+// d = older + d (the older, left operand first; IEEE addition is commutative,
+// the order of the operands is kept only for clarity)
+template <int U, int V> __device__ __forceinline__ void add_left(Acc<U, V>& d, const Acc<U, V>& older) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < V; ++i) d.a[u][i] = older.a[u][i] + d.a[u][i];
+}
+
+// d = d + x
+template <int U, int V> __device__ __forceinline__ void add_right(Acc<U, V>& d, const Acc<U, V>& x) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < V; ++i) d.a[u][i] = d.a[u][i] + x.a[u][i];
+}
+
+// Replica k's vectors of this lane: the replica pointer comes from the plan's
+// table (scalar load), the tile start is added in scalar registers.
+template <int DT, int V, int U, bool NT>
+__device__ __forceinline__ void load_leaf(const void* const* grads, int k, uint64_t start_bytes,
+                                          const uint32_t (&off)[U], typename Rep<DT, V>::raw (&r)[U]) {
+    const gptr_t base = gread(ldc(grads, k)) + start_bytes;
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = Rep<DT, V>::template load<NT>(base, off[u]);
+}
+
+template <int DT, int V, int U>
+__device__ __forceinline__ void widen_leaf(Acc<U, V>& x, const typename Rep<DT, V>::raw (&r)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) Rep<DT, V>::widen(r[u], x.a[u]);
+}
+
+// Binary-counter push of subtree p as subtree number `n` (0-based) onto the
+// pending stack st[0..D-1]: for every bit d below the lowest clear bit t of n,
+// the pending subtree st[d] (older, same size) is merged on the left; p then
+// waits in st[t].  Requires n <= 2^D - 2 so that t < D.  Every branch is
+// uniform and every index a constant, so the stack stays in registers.
+template <int D, int U, int V>
+__device__ __forceinline__ void push(Acc<U, V> (&st)[D], Acc<U, V>& p, int n) {
+    const int t = __builtin_ctz(~static_cast<unsigned>(n));
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        if (d < t) add_left(p, st[d]);
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        const bool here = d == t;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < V; ++i) st[d].a[u][i] = here ? p.a[u][i] : st[d].a[u][i];
+    }
+}
+
+// Fold the pending subtrees named by the set bits of n into acc, newest
+// (lowest bit) first, each older subtree on the left.  `have` says whether
+// acc already holds a partial sum.
+template <int D, int U, int V>
+__device__ __forceinline__ void fold(const Acc<U, V> (&st)[D], int n, Acc<U, V>& acc, bool& have) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        const bool take = (n >> d) & 1;
+        const bool merge = take && have;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const float sum = st[d].a[u][i] + acc.a[u][i];
+                acc.a[u][i] = merge ? sum : (take ? st[d].a[u][i] : acc.a[u][i]);
+            }
+        have = have || take;
+    }
+}
+
+// Sum over the K replicas of V elements at e[u], u < U, in tree or linear order.
+template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT>
+__device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t start_bytes,
+                                       const uint32_t (&off)[U], Acc<U, V>& acc) {
+    typedef typename Rep<DT, V>::raw raw_t;
+    const int nfull = K / C;  // whole chunks of C consecutive replicas
+    const int r = K - nfull * C;
+    bool have = false;  // uniform across the block
+
+    if constexpr (TREE) {
+        Acc<U, V> st[MAXD];  // st[d]: pending balanced subtree of C * 2^d leaves
+        for (int c = 0; c < nfull; ++c) {
+            raw_t raw[C][U];
+#pragma unroll
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, NT>(grads, c * C + j, start_bytes, off, raw[j]);
+            Acc<U, V> x[C];
+#pragma unroll
+            for (int j = 0; j < C; ++j) widen_leaf<DT, V, U>(x[j], raw[j]);
+            // balanced subtree over the chunk, level by level: x[m] = x[2m] + x[2m+1]
+#pragma unroll
+            for (int h = C / 2; h >= 1; h /= 2) {
+#pragma unroll
+                for (int m = 0; m < h; ++m) {
+                    add_right(x[2 * m], x[2 * m + 1]);
+                    if (m) set(x[m], x[2 * m]);
+                }
+            }
+            push<MAXD>(st, x[0], c);
+        }
+        if (r) {
+            constexpr int LC = ilog2<C>();
+            raw_t raw[C - 1][U];
+#pragma unroll
+            for (int i = 0; i < C - 1; ++i)
+                if (i < r) load_leaf<DT, V, U, NT>(grads, nfull * C + i, start_bytes, off, raw[i]);
+            Acc<U, V> rs[LC];
+#pragma unroll
+            for (int i = 0; i < C - 1; ++i) {
+                if (i < r) {
+                    Acc<U, V> p;
+                    widen_leaf<DT, V, U>(p, raw[i]);
+                    push<LC>(rs, p, i);
+                }
+            }
+            // the remainder's pending subtrees are the newest: fold them first
+            fold<LC>(rs, r, acc, have);
+        }
+        fold<MAXD>(st, nfull, acc, have);
+    } else {
+        for (int c = 0; c < nfull; ++c) {
+            raw_t raw[C][U];
+#pragma unroll
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, NT>(grads, c * C + j, start_bytes, off, raw[j]);
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                Acc<U, V> x;
+                widen_leaf<DT, V, U>(x, raw[j]);
+                if (have) add_right(acc, x);
+                else set(acc, x);
+                have = true;
+            }
+        }
+        if (r) {
+            raw_t raw[C - 1][U];
+#pragma unroll
+            for (int i = 0; i < C - 1; ++i)
+                if (i < r) load_leaf<DT, V, U, NT>(grads, nfull * C + i, start_bytes, off, raw[i]);
+#pragma unroll
+            for (int i = 0; i < C - 1; ++i) {
+                if (i < r) {
+                    Acc<U, V> x;
+                    widen_leaf<DT, V, U>(x, raw[i]);
+                    if (have) add_right(acc, x);
+                    else set(acc, x);
+                    have = true;
+                }
+            }
+        }
+    }
+}
+
+// One element of the momentum-SGD update; six rounded fp32 operations.
+__device__ __forceinline__ void sgd1(float s, float w, float v, float lr_j, float mu, float wd_j,
+                                     float c, float& wn, float& vn) {
+    const float ga = s * c;
+    const float decay = wd_j * w;
+    const float d = ga + decay;
+    const float mom = mu * v;
+    const float step = lr_j * d;
+    vn = mom + step;
+    wn = w - vn;
+}
+
+// Lane layout inside a tile: vector u of lane t is tile vector t + u*blockDim.
+// Inactive lanes point at vector 0 of the tile (always valid) and store
+// nothing.  idx[u] is the lane's element index relative to the tile start.
+template <int V, int U>
+__device__ __forceinline__ void lane_elems(uint32_t count, uint32_t (&idx)[U], bool (&act)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t vi = threadIdx.x + u * blockDim.x;
+        act[u] = vi < count;
+        idx[u] = (act[u] ? vi : 0u) * V;
+    }
+}
+
+template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT, int MODE>
+__device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start, uint32_t count,
+                                            float lr_j, float wd_j) {
+    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
+    uint32_t idx[U], roff[U], off[U];
+    bool act[U];
+    lane_elems<V, U>(count, idx, act);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        roff[u] = idx[u] * SG;
+        off[u] = idx[u] * 4;
+    }
+    const uint64_t start4 = start * 4;
+    float w[U][V], v[U][V];
+    if constexpr (MODE == MODE_STEP) {
+        // issue the weight and velocity loads before the replica stream
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ld32<V>(gread(a.w) + start4, off[u], w[u]);
+            ld32<V>(gread(a.v) + start4, off[u], v[u]);
+        }
+    }
+    Acc<U, V> s;
+    reduce<DT, V, U, C, MAXD, TREE, NT>(a.grads, a.K, start * SG, roff, s);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!act[u]) continue;
+        if constexpr (MODE == MODE_REDUCE) {
+            st32<V>(gwrite(a.out) + start4, off[u], s.a[u]);
+        } else {
+            float wn[V], vn[V];
+#pragma unroll
+            for (int i = 0; i < V; ++i) sgd1(s.a[u][i], w[u][i], v[u][i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
+            st32<V>(gwrite(a.w) + start4, off[u], wn);
+            st32<V>(gwrite(a.v) + start4, off[u], vn);
+            if (a.out) st32<V>(gwrite(a.out) + start4, off[u], s.a[u]);
+            if (a.dst)
+                for (int k = 0; k < a.K; ++k) st32<V>(gwrite(ldc(a.dst, k)) + start4, off[u], wn);
+        }
+    }
+}
+
+template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT, int MODE>
+__global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
+    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+        const Tile tile = ld_tile(a.tiles, t);
+        float lr_j = 0.0f, wd_j = 0.0f;
+        if constexpr (MODE == MODE_STEP) {
+            const int j = static_cast<int>(tile.seg & SEG_MASK);
+            lr_j = a.lr * ldc(a.mults, 2 * j);
+            wd_j = a.wd * ldc(a.mults, 2 * j + 1);
+        }
+        if (!(tile.seg & TAIL_BIT))
+            reduce_body<DT, V, U, C, MAXD, TREE, NT, MODE>(a, tile.start, tile.count, lr_j, wd_j);
+        else
+            reduce_body<DT, 1, 1, C, MAXD, TREE, NT, MODE>(a, tile.start, tile.count, lr_j, wd_j);
+    }
+}
+
+// ------------------------------------------------------------------ SGD from a raw sum
+template <int V, int U>
+__device__ __forceinline__ void sgd_body(const SgdArgs& a, uint64_t start, uint32_t count, float lr_j,
+                                         float wd_j) {
+    uint32_t idx[U];
+    bool act[U];
+    lane_elems<V, U>(count, idx, act);
+    const uint64_t start4 = start * 4;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!act[u]) continue;
+        const uint32_t off = idx[u] * 4;
+        float g[V], w[V], v[V], wn[V], vn[V];
+        ld32<V>(gread(a.g) + start4, off, g);
+        ld32<V>(gread(a.w) + start4, off, w);
+        ld32<V>(gread(a.v) + start4, off, v);
+#pragma unroll
+        for (int i = 0; i < V; ++i) sgd1(g[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
+        st32<V>(gwrite(a.w) + start4, off, wn);
+        st32<V>(gwrite(a.v) + start4, off, vn);
+    }
+}
+
+template <int V, int U>
+__global__ __launch_bounds__(256) void sgd_kernel(SgdArgs a) {
+    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+        const Tile tile = ld_tile(a.tiles, t);
+        const int j = static_cast<int>(tile.seg & SEG_MASK);
+        const float lr_j = a.lr * ldc(a.mults, 2 * j);
+        const float wd_j = a.wd * ldc(a.mults, 2 * j + 1);
+        if (!(tile.seg & TAIL_BIT)) sgd_body<V, U>(a, tile.start, tile.count, lr_j, wd_j);
+        else sgd_body<1, 1>(a, tile.start, tile.count, lr_j, wd_j);
+    }
+}
+
+// ------------------------------------------------------------------ broadcast
+template <int V, int U>
+__device__ __forceinline__ void bcast_body(const BcastArgs& a, uint64_t start, uint32_t count) {
+    uint32_t idx[U];
+    bool act[U];
+    lane_elems<V, U>(count, idx, act);
+    const uint64_t start4 = start * 4;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!act[u]) continue;
+        const uint32_t off = idx[u] * 4;
+        float x[V];
+        ld32<V>(gread(a.src) + start4, off, x);
+        for (int k = 0; k < a.K; ++k) st32<V>(gwrite(ldc(a.dst, k)) + start4, off, x);
+    }
+}
+
+template <int V, int U>
+__global__ __launch_bounds__(256) void bcast_kernel(BcastArgs a) {
+    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+        const Tile tile = ld_tile(a.tiles, t);
+        if (!(tile.seg & TAIL_BIT)) bcast_body<V, U>(a, tile.start, tile.count);
+        else bcast_body<1, 1>(a, tile.start, tile.count);
+    }
+}
+
+// ------------------------------------------------------------------ dispatch
+template <int N> using I = std::integral_constant<int, N>;
+
+template <int A, int B, class F> hipError_t pick(int x, F&& f) {
+    return x == B ? f(I<B>{}) : f(I<A>{});
+}
+
+template <int DT, int TREE, int MODE, int U, int C, int MAXD, int NT>
+hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
+    constexpr int V = DT == FC_F16 ? 8 : 4;
+    hipLaunchKernelGGL((reduce_kernel<DT, V, U, C, MAXD, (TREE != 0), (NT != 0), MODE>), dim3(grid),
+                       dim3(block), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_reduce(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
+    return pick<FC_F32, FC_F16>(sh.dtype, [&](auto dt) {
+        return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
+            return pick<1, 2>(sh.vecs, [&](auto u) {
+                return pick<8, 16>(sh.kchunk, [&](auto c) {
+                    return pick<0, 1>(sh.nontemporal, [&](auto nt) {
+                        if (sh.tree) {
+                            return pick<MAXD_SMALL, MAXD_LARGE>(sh.maxd, [&](auto d) {
+                                return go_reduce<dt.value, 1, md.value, u.value, c.value, d.value, nt.value>(
+                                    grid, sh.block, a, s);
+                            });
+                        }
+                        return go_reduce<dt.value, 0, md.value, u.value, c.value, 1, nt.value>(grid, sh.block,
+                                                                                                a, s);
+                    });
+                });
+            });
+        });
+    });
+}
+
+hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s) {
+    return pick<4, 8>(sh.dtype == FC_F16 ? 8 : 4, [&](auto v) {
+        return pick<1, 2>(sh.vecs, [&](auto u) {
+            hipLaunchKernelGGL((sgd_kernel<v.value, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
+            return hipGetLastError();
+        });
+    });
+}
+
+hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s) {
+    return pick<4, 8>(sh.dtype == FC_F16 ? 8 : 4, [&](auto v) {
+        return pick<1, 2>(sh.vecs, [&](auto u) {
+            hipLaunchKernelGGL((bcast_kernel<v.value, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
+            return hipGetLastError();
+        });
+    });
+}
+
+}  // namespace fc

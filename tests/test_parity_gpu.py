@@ -1,0 +1,218 @@
+"""HIP path vs the oracle, bit for bit, through the C ABI.
+
+Sizes: ragged random segment tables of a few tens of thousands of elements
+(several tiles per segment, lengths that are not multiples of the vector
+width, tiny segments) so the oracle finishes in well under a second per case.
+Tolerance: none -- the reduced sums and the SGD update are compared bit for
+bit (NaN compared as NaN), because both sides perform the same fp32
+operations in the same order with no contraction.
+"""
+import numpy as np
+import pytest
+
+from gpu_cases import run_reduce, run_steps, same_bits, to_dev
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fc(device):
+    import paper_1511_00175_amd as m
+    return m
+
+
+def table(seed, dtype, nseg=9, max_len=5000):
+    rng = np.random.default_rng(seed)
+    vec = 8 if dtype == "f16" else 4
+    rows, _ = gen.random_table(rng, nseg, max_len, vec)
+    # a tiny segment, one exactly one default tile long, one a tile plus one
+    off = rows[-1][0] + rows[-1][1]
+    off = (off + vec - 1) // vec * vec
+    for n in (3, 256 * vec, 256 * vec + 1, 16):
+        rows.append((off, n, 1.0, 1.0))
+        off = (off + n + 63) // 64 * 64
+    return rows
+
+
+KS = [1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 17, 31, 32, 33, 64, 100, 128]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("order", ["tree", "linear"])
+@pytest.mark.parametrize("K", KS)
+def test_reduce_matches_oracle(fc, K, order, dtype):
+    segs = table(1000 + K, dtype)
+    bad, _, _ = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(K))
+    assert bad == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("order", ["tree", "linear"])
+@pytest.mark.parametrize("K", KS)
+def test_step_matches_oracle(fc, K, order, dtype):
+    segs = [(o, n, lm, dm) for (o, n, lm, dm) in table(2000 + K, dtype)]
+    # non-uniform multipliers on some segments (Caffe-style bias settings)
+    segs = [(o, n, 2.0, 0.0) if i % 3 == 1 else (o, n, lm, dm) for i, (o, n, lm, dm) in enumerate(segs)]
+    assert run_steps(fc, segs, K, dtype, order, np.random.default_rng(K), steps=3) == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("K", [1, 3, 8, 32, 100])
+def test_step_with_sum_and_broadcast(fc, K, dtype):
+    segs = table(3000 + K, dtype, nseg=5, max_len=3000)
+    assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(K), steps=2, with_out=True,
+                     with_bcast=True) == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("order", ["tree", "linear"])
+@pytest.mark.parametrize("K", [1, 2, 5, 16, 33])
+def test_special_values(fc, K, order, dtype):
+    """Signed zeros, subnormals of the storage type, infinities and NaN."""
+    segs = table(4000 + K, dtype, nseg=4, max_len=2000)
+    bad, _, _ = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(K), special=True)
+    assert bad == 0
+    assert run_steps(fc, segs, K, dtype, order, np.random.default_rng(K), steps=2, special=True) == 0
+
+
+@pytest.mark.parametrize("K", [256, 1000, 1024])
+def test_many_workers(fc, K):
+    """K beyond 31 chunks uses the deeper pending-subtree stack."""
+    segs = [(0, 1000, 1, 1), (1024, 37, 1, 1), (1088, 8, 1, 1)]
+    for dtype in ("f32", "f16"):
+        for order in ("tree", "linear"):
+            bad, _, _ = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(K))
+            assert bad == 0, (dtype, order)
+    assert run_steps(fc, segs, K, "f32", "tree", np.random.default_rng(K), steps=1) == 0
+
+
+def test_fp16_widening_exhaustive(fc):
+    """All 65536 binary16 patterns as one K=1 replica: the sum is the widened
+    value (numpy's float16->float32 conversion, a library routine)."""
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ref = bits.view(np.float16).astype(np.float32)
+    plan = fc.Plan([(0, 1 << 16)], 1, "f16", "tree")
+    out = torch.zeros(1 << 16, device="cuda")
+    plan.tree_reduce([to_dev(bits.view(np.float16))], out)
+    assert same_bits(out.cpu().numpy(), ref) == 0
+
+
+SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c, nontemporal=nt)
+          for b in (64, 128, 256) for u in (1, 2) for c in (8, 16) for nt in (0, 1)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_launch_shape_invariance(fc, dtype):
+    """Identical bits for every launch shape (and a capped grid that makes
+    blocks loop over tiles) -- the association never depends on it."""
+    segs = table(5000, dtype)
+    K = 37
+    ref = None
+    for opts in SHAPES + [dict(max_blocks=7), dict(max_blocks=1, vecs_per_thread=2)]:
+        bad, got, expect = run_reduce(fc, segs, K, dtype, "tree", np.random.default_rng(5), opts=opts)
+        assert bad == 0, opts
+        if ref is None:
+            ref = got
+        assert same_bits(got, ref) == 0
+        assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(6), steps=1, opts=opts) == 0, opts
+
+
+def test_fused_equals_composed(fc):
+    """fc_step == fc_tree_reduce, then fc_sgd_step, then fc_broadcast of w'."""
+    import torch
+    rng = np.random.default_rng(7)
+    segs = table(7000, "f32")
+    K = 24
+    n = max(o + ln for o, ln, _, _ in segs) + 64
+    reps = to_dev((rng.standard_normal((K, n)) * 1e-2).astype(np.float32))
+    w0 = to_dev((rng.standard_normal(n) * 0.05).astype(np.float32))
+    v0 = to_dev((rng.standard_normal(n) * 1e-3).astype(np.float32))
+    plan = fc.Plan(segs, K, "f32", "tree")
+    w1, v1, out1 = w0.clone(), v0.clone(), torch.zeros(n, device="cuda")
+    d1 = torch.zeros((K, n), device="cuda")
+    plan.step(reps, w1, v1, 0.02, 0.9, 1e-4, 128, out=out1, bcast=d1)
+    w2, v2, g = w0.clone(), v0.clone(), torch.zeros(n, device="cuda")
+    d2 = torch.zeros((K, n), device="cuda")
+    plan.tree_reduce(reps, g)
+    plan.sgd_step(w2, v2, g, 0.02, 0.9, 1e-4, 128)
+    plan.broadcast(w2, d2)
+    torch.cuda.synchronize()
+    for a, b in ((w1, w2), (v1, v2), (out1, g), (d1, d2)):
+        assert same_bits(a.cpu().numpy(), b.cpu().numpy()) == 0
+
+
+def test_repeatable(fc):
+    """The same inputs give the same bits on every run (FAQ 6: no
+    nondeterministic techniques)."""
+    segs = table(8000, "f32")
+    r1 = run_reduce(fc, segs, 64, "f32", "tree", np.random.default_rng(3))[1]
+    for _ in range(3):
+        r2 = run_reduce(fc, segs, 64, "f32", "tree", np.random.default_rng(3))[1]
+        assert same_bits(r1, r2) == 0
+
+
+def test_out_may_be_a_replica(fc):
+    """out == grads[k] exactly is allowed for fp32 replicas and gives the sum."""
+    import oracle
+    import torch
+    rng = np.random.default_rng(9)
+    segs = [(0, 4000, 1, 1), (4096, 77, 1, 1)]
+    K, n = 6, 4224
+    reps = (rng.standard_normal((K, n))).astype(np.float32)
+    expect = oracle.tree_reduce(segs, list(reps), out=reps[2].copy())
+    plan = fc.Plan(segs, K, "f32", "tree")
+    rd = to_dev(reps)
+    plan.tree_reduce(rd, rd[2])
+    torch.cuda.synchronize()
+    assert same_bits(rd[2].cpu().numpy(), expect) == 0
+
+
+def test_argument_errors_need_a_plan(fc):
+    import torch
+    f = fc._fc
+    plan = fc.Plan([(0, 1000, 1, 1)], 4, "f32", "tree")
+    buf = torch.zeros(8192, device="cuda")
+    reps = [buf[i * 1024:].data_ptr() for i in range(4)]
+    out = torch.zeros(1024, device="cuda")
+    w = torch.zeros(1024, device="cuda")
+    v = torch.zeros(1024, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    h = plan.handle
+    # misaligned pointers
+    assert f.fc_tree_reduce(h, reps, out.data_ptr() + 4, s) == f.FC_EALIGN
+    assert f.fc_tree_reduce(h, [reps[0] + 8] + reps[1:], out.data_ptr(), s) == f.FC_EALIGN
+    # null replica
+    assert f.fc_tree_reduce(h, [0] + reps[1:], out.data_ptr(), s) == f.FC_EINVAL
+    # out partially overlapping a replica
+    assert f.fc_tree_reduce(h, reps, reps[1] + 16, s) == f.FC_EALIAS
+    # w == v, v overlapping g
+    assert f.fc_sgd_step(h, w.data_ptr(), w.data_ptr(), out.data_ptr(), 0.1, 0.9, 0.0, 1, s) == f.FC_EALIAS
+    assert f.fc_sgd_step(h, w.data_ptr(), out.data_ptr() + 16, out.data_ptr(), 0.1, 0.9, 0.0, 1, s) == f.FC_EALIAS
+    assert f.fc_sgd_step(h, w.data_ptr(), v.data_ptr(), out.data_ptr(), 0.1, 0.9, 0.0, 0, s) == f.FC_EINVAL
+    # broadcast destinations overlapping each other or the source
+    dst = [buf[4096 + 1024 * i:].data_ptr() for i in range(4)]
+    assert f.fc_broadcast(h, out.data_ptr(), dst[:3] + [dst[2]], s) == f.FC_EALIAS
+    assert f.fc_broadcast(h, dst[0], dst, s) == f.FC_EALIAS
+    # a broadcast destination overlapping w
+    assert f.fc_step(h, reps, w.data_ptr(), v.data_ptr(), 0.1, 0.9, 0.0, 1, None, dst[:3] + [w.data_ptr()],
+                     s) == f.FC_EALIAS
+    torch.cuda.synchronize()
+    # nothing was written by the rejected calls
+    assert float(out.abs().sum()) == 0.0 and float(w.abs().sum()) == 0.0
+
+
+def test_empty_and_zero_length(fc):
+    import torch
+    plan = fc.Plan([], 3, "f32", "tree")
+    assert plan.info().ntiles == 0
+    x = torch.zeros((3, 64), device="cuda")
+    w, v = torch.ones(64, device="cuda"), torch.ones(64, device="cuda")
+    plan.step(x, w, v, 0.1, 0.9, 0.1, 1)
+    plan.tree_reduce(x, w)
+    torch.cuda.synchronize()
+    assert float(w.sum()) == 64.0
+    segs = [(0, 0, 1, 1), (8, 5, 1, 1), (16, 0, 1, 1)]
+    bad, got, _ = run_reduce(fc, segs, 3, "f32", "tree", np.random.default_rng(1))
+    assert bad == 0
