@@ -87,10 +87,10 @@ typedef struct fc_plan fc_plan;
  * fields only change speed.  Zero (or -1 for `nontemporal`) selects the
  * default. */
 typedef struct {
-    int block_threads;   /* 64, 128 or 256 threads per block (default 256) */
-    int vecs_per_thread; /* 16-byte vectors per thread per replica: 1 or 2 (default 1) */
-    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 8) */
-    int nontemporal;     /* 1: replica loads carry the non-temporal hint; 0: plain loads */
+    int block_threads;   /* 64, 128 or 256 threads per block (default 64 fp32, 256 fp16) */
+    int vecs_per_thread; /* 16-byte vectors per thread per replica: 1 or 2 (default 1 fp32, 2 fp16) */
+    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 16 fp32, 8 fp16) */
+    int nontemporal;     /* 1: replica loads carry the streaming (nt) hint (default); 0: plain loads */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
 } fc_launch_opts;
 

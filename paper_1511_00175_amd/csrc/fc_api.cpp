@@ -106,11 +106,16 @@ void note_stream(fc_plan* p, hipStream_t s) {
     p->have_last_stream = true;
 }
 
-int validate_opts(const fc_launch_opts* o, fc::Shape& sh) {
-    sh.block = 256;
-    sh.vecs = 1;
-    sh.kchunk = 8;
-    sh.nontemporal = 0;
+int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc::Shape& sh) {
+    // Defaults measured best on MI355X: fp32 replicas -- 64-thread blocks,
+    // one 16-byte vector per lane, 16 replicas per batch; fp16 replicas (8
+    // elements per vector, twice the accumulator registers) -- 256-thread
+    // blocks, two vectors per lane, 8 replicas per batch.  Replica loads
+    // stream (nt) in both cases.
+    sh.block = gdt == FC_F16 ? 256 : 64;
+    sh.vecs = gdt == FC_F16 ? 2 : 1;
+    sh.kchunk = gdt == FC_F16 ? 8 : 16;
+    sh.nontemporal = 1;
     if (!o) return FC_OK;
     if (o->block_threads) {
         if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
@@ -175,7 +180,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     if (gdt != FC_F32 && gdt != FC_F16) return FC_EINVAL;
     if (order != FC_ORDER_TREE && order != FC_ORDER_LINEAR) return FC_EINVAL;
     fc::Shape sh{};
-    int rc = validate_opts(opts, sh);
+    int rc = validate_opts(opts, gdt, sh);
     if (rc) return rc;
 
     const int vec = gdt == FC_F16 ? 8 : 4;

@@ -69,6 +69,21 @@ __device__ __forceinline__ Tile ld_tile(const Tile* tiles, int t) {
 __device__ __forceinline__ gptr_t gread(const void* p) { return (gptr_t)p; }
 __device__ __forceinline__ gptr_w_t gwrite(void* p) { return (gptr_w_t)p; }
 
+// Cache-policy bits of gfx950 buffer instructions: bit 0 = sc0, bit 1 = nt,
+// bit 4 = sc1.  Replicas are read once, so their loads carry nt (streaming).
+// Result stores carry sc1: measured on MI355X, this keeps the written lines
+// from competing with the replica stream and is what lets two result streams
+// (w' and v') ride along a 128-stream read at little cost.
+constexpr int CPOL_STREAM_LOAD = 2;   // nt
+constexpr int CPOL_RESULT_STORE = 16; // sc1
+
+// Raw buffer resource over [base, base + 2 GiB): word 3 = 0x00020000 is the
+// gfx9 data-format field for untyped 32-bit access.  Offsets used here are
+// lane offsets within one tile (a few KiB).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+
 // ------------------------------------------------------------------ replica loads
 // Rep<DT, V>: V consecutive replica elements starting at element e.
 template <int DT, int V> struct Rep;
@@ -78,9 +93,12 @@ template <int DT, int V> struct Rep;
 template <> struct Rep<FC_F32, 4> {
     typedef f4 raw;
     template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        const FC_GLOBAL f4* q = reinterpret_cast<const FC_GLOBAL f4*>(base + off);
-        if constexpr (NT) return __builtin_nontemporal_load(q);
-        else return *q;
+        if constexpr (NT) {
+            return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
+                                                                               CPOL_STREAM_LOAD));
+        } else {
+            return *reinterpret_cast<const FC_GLOBAL f4*>(base + off);
+        }
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
         x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
@@ -101,9 +119,12 @@ template <> struct Rep<FC_F32, 1> {
 template <> struct Rep<FC_F16, 8> {
     typedef u4 raw;
     template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        const FC_GLOBAL u4* q = reinterpret_cast<const FC_GLOBAL u4*>(base + off);
-        if constexpr (NT) return __builtin_nontemporal_load(q);
-        else return *q;
+        if constexpr (NT) {
+            return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
+                                                                               CPOL_STREAM_LOAD));
+        } else {
+            return *reinterpret_cast<const FC_GLOBAL u4*>(base + off);
+        }
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
         const h8 h = __builtin_bit_cast(h8, r);
@@ -125,28 +146,34 @@ template <> struct Rep<FC_F16, 1> {
 };
 
 // ------------------------------------------------------------------ fp32 vectors
-// V consecutive fp32 values at byte offset `off` from the uniform base.
-template <int V> __device__ __forceinline__ void ld32(gptr_t base, uint32_t off, float* x) {
+// V fp32 results at byte offset `off`, stored with the result-store policy
+template <int V> __device__ __forceinline__ void st32r(gptr_w_t base, uint32_t off, const float* x) {
     if constexpr (V == 1) {
-        x[0] = *reinterpret_cast<const FC_GLOBAL float*>(base + off);
-    } else {
-#pragma unroll
-        for (int q = 0; q < V / 4; ++q) {
-            const f4 t = *reinterpret_cast<const FC_GLOBAL f4*>(base + off + 16 * q);
-            x[4 * q + 0] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
-        }
-    }
-}
-
-template <int V> __device__ __forceinline__ void st32(gptr_w_t base, uint32_t off, const float* x) {
-    if constexpr (V == 1) {
-        *reinterpret_cast<FC_GLOBAL float*>(base + off) = x[0];
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x[0]), rsrc((const void*)base), off, 0,
+                                              CPOL_RESULT_STORE);
     } else {
 #pragma unroll
         for (int q = 0; q < V / 4; ++q) {
             f4 t;
             t.x = x[4 * q + 0]; t.y = x[4 * q + 1]; t.z = x[4 * q + 2]; t.w = x[4 * q + 3];
-            *reinterpret_cast<FC_GLOBAL f4*>(base + off + 16 * q) = t;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, t), rsrc((const void*)base), off + 16 * q, 0,
+                                                   CPOL_RESULT_STORE);
+        }
+    }
+}
+
+// V fp32 values at byte offset `off`, read once (streaming policy)
+template <int V> __device__ __forceinline__ void ld32s(gptr_t base, uint32_t off, float* x) {
+    if constexpr (V == 1) {
+        x[0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc((const void*)base), off, 0,
+                                                                            CPOL_STREAM_LOAD));
+    } else {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            const f4 t = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base),
+                                                                                     off + 16 * q, 0,
+                                                                                     CPOL_STREAM_LOAD));
+            x[4 * q + 0] = t.x; x[4 * q + 1] = t.y; x[4 * q + 2] = t.z; x[4 * q + 3] = t.w;
         }
     }
 }
@@ -359,31 +386,32 @@ __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start,
         off[u] = idx[u] * 4;
     }
     const uint64_t start4 = start * 4;
-    float w[U][V], v[U][V];
-    if constexpr (MODE == MODE_STEP) {
-        // issue the weight and velocity loads before the replica stream
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            ld32<V>(gread(a.w) + start4, off[u], w[u]);
-            ld32<V>(gread(a.v) + start4, off[u], v[u]);
-        }
-    }
     Acc<U, V> s;
     reduce<DT, V, U, C, MAXD, TREE, NT>(a.grads, a.K, start * SG, roff, s);
+    if constexpr (MODE == MODE_REDUCE) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        if (!act[u]) continue;
-        if constexpr (MODE == MODE_REDUCE) {
-            st32<V>(gwrite(a.out) + start4, off[u], s.a[u]);
-        } else {
+        for (int u = 0; u < U; ++u)
+            if (act[u]) st32r<V>(gwrite(a.out) + start4, off[u], s.a[u]);
+    } else {
+        // weights and velocity are read after the replica stream: loading them
+        // first only holds registers while the sums are being formed
+        float w[U][V], v[U][V];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ld32s<V>(gread(a.w) + start4, off[u], w[u]);
+            ld32s<V>(gread(a.v) + start4, off[u], v[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!act[u]) continue;
             float wn[V], vn[V];
 #pragma unroll
             for (int i = 0; i < V; ++i) sgd1(s.a[u][i], w[u][i], v[u][i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
-            st32<V>(gwrite(a.w) + start4, off[u], wn);
-            st32<V>(gwrite(a.v) + start4, off[u], vn);
-            if (a.out) st32<V>(gwrite(a.out) + start4, off[u], s.a[u]);
+            st32r<V>(gwrite(a.w) + start4, off[u], wn);
+            st32r<V>(gwrite(a.v) + start4, off[u], vn);
+            if (a.out) st32r<V>(gwrite(a.out) + start4, off[u], s.a[u]);
             if (a.dst)
-                for (int k = 0; k < a.K; ++k) st32<V>(gwrite(ldc(a.dst, k)) + start4, off[u], wn);
+                for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off[u], wn);
         }
     }
 }
@@ -418,13 +446,13 @@ __device__ __forceinline__ void sgd_body(const SgdArgs& a, uint64_t start, uint3
         if (!act[u]) continue;
         const uint32_t off = idx[u] * 4;
         float g[V], w[V], v[V], wn[V], vn[V];
-        ld32<V>(gread(a.g) + start4, off, g);
-        ld32<V>(gread(a.w) + start4, off, w);
-        ld32<V>(gread(a.v) + start4, off, v);
+        ld32s<V>(gread(a.g) + start4, off, g);
+        ld32s<V>(gread(a.w) + start4, off, w);
+        ld32s<V>(gread(a.v) + start4, off, v);
 #pragma unroll
         for (int i = 0; i < V; ++i) sgd1(g[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
-        st32<V>(gwrite(a.w) + start4, off, wn);
-        st32<V>(gwrite(a.v) + start4, off, vn);
+        st32r<V>(gwrite(a.w) + start4, off, wn);
+        st32r<V>(gwrite(a.v) + start4, off, vn);
     }
 }
 
@@ -452,8 +480,8 @@ __device__ __forceinline__ void bcast_body(const BcastArgs& a, uint64_t start, u
         if (!act[u]) continue;
         const uint32_t off = idx[u] * 4;
         float x[V];
-        ld32<V>(gread(a.src) + start4, off, x);
-        for (int k = 0; k < a.K; ++k) st32<V>(gwrite(ldc(a.dst, k)) + start4, off, x);
+        ld32s<V>(gread(a.src) + start4, off, x);
+        for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, x);
     }
 }
 
