@@ -27,12 +27,16 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD published peak
 METRIC = "effective HBM GB/s (and % of peak) for tree-reduce+SGD step; µs per step"
-KERNEL_SRC = os.path.join(ROOT, "paper_1511_00175_amd", "csrc", "fc_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_1511_00175_amd", "csrc")
 
 
 def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the HIP library sources (kernels and launch defaults)."""
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, fn), "rb") as f:
+            h.update(fn.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def read_traffic(workload):
@@ -130,8 +134,15 @@ def main():
     ap.add_argument("--opts", default="", help="launch shape, e.g. block_threads=256,vecs_per_thread=1")
     ap.add_argument("--profile-loop", type=int, default=0,
                     help="after the measurement, launch this many extra steps (for rocprofv3 runs)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the measurement, run a plain device copy of this many MiB three times "
+                         "(reference kernel of known size for hardware byte counters)")
+    ap.add_argument("--print-hash", action="store_true", help="print the library source hash and exit")
     args = ap.parse_args()
 
+    if args.print_hash:
+        print(kernel_hash())
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: this build measures one GPU only (the K workers are replicas on one device); "
@@ -182,6 +193,14 @@ def main():
     for _ in range(args.profile_loop):
         step()
     torch.cuda.synchronize()
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, device=dev)
+        dst = torch.empty(n, device=dev)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     bytes_step = wl.algorithmic_bytes(out=args.out, bcast=args.bcast)
     ms_per_step = wall / args.steps * 1e3

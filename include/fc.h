@@ -55,7 +55,7 @@ extern "C" {
 #define FC_OK 0
 #define FC_EINVAL (-1) /* bad argument: null pointer, K out of range, bad table, batch < 1 */
 #define FC_EALIGN (-2) /* pointer not 16-byte aligned, or a segment offset not a multiple of
-                          the replica vector width (4 elements fp32, 8 elements fp16) */
+                          4 elements */
 #define FC_EALIAS (-3) /* a written buffer overlaps another buffer (see each call) */
 #define FC_EHIP (-4)   /* the HIP runtime reported an error (allocation, copy or launch) */
 #define FC_ENOMEM (-5) /* host allocation failed */
@@ -87,9 +87,9 @@ typedef struct fc_plan fc_plan;
  * fields only change speed.  Zero (or -1 for `nontemporal`) selects the
  * default. */
 typedef struct {
-    int block_threads;   /* 64, 128 or 256 threads per block (default 64 fp32, 256 fp16) */
-    int vecs_per_thread; /* 16-byte vectors per thread per replica: 1 or 2 (default 1 fp32, 2 fp16) */
-    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 16 fp32, 8 fp16) */
+    int block_threads;   /* 64, 128 or 256 threads per block (default 64) */
+    int vecs_per_thread; /* 4-element lane-vectors per thread: 1 or 2 (default 1 fp32, 2 fp16) */
+    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 16) */
     int nontemporal;     /* 1: replica loads carry the streaming (nt) hint (default); 0: plain loads */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
 } fc_launch_opts;
@@ -97,7 +97,7 @@ typedef struct {
 /* Create a plan for K workers over a segment table (Sec. 6: one gradient
  * vector per worker).  segs[0..nseg-1] is copied; nseg may be 0 (every call
  * then does nothing).  1 <= K <= 1024.  Offsets must be multiples of 4
- * elements (FC_F32) or 8 elements (FC_F16).  Allocates the plan's device
+ * elements (16 bytes of fp32, 8 bytes of fp16).  Allocates the plan's device
  * tables on the current device with hipMalloc (FC_EHIP on failure).
  * On success *plan receives the plan; on failure *plan is set to NULL. */
 int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,

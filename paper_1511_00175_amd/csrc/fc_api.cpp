@@ -19,7 +19,7 @@ struct fc_plan {
     int K = 0;
     fc_dtype gdt = FC_F32;
     fc_order order = FC_ORDER_TREE;
-    int vec = 4;        // elements per 16-byte replica vector
+    int vec = 4;        // elements per lane-vector (16 bytes of fp32, 8 bytes of fp16)
     int sg = 4;         // bytes per replica element
     std::vector<fc_segment> segs;
     uint64_t n_elems = 0;
@@ -107,14 +107,12 @@ void note_stream(fc_plan* p, hipStream_t s) {
 }
 
 int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc::Shape& sh) {
-    // Defaults measured best on MI355X: fp32 replicas -- 64-thread blocks,
-    // one 16-byte vector per lane, 16 replicas per batch; fp16 replicas (8
-    // elements per vector, twice the accumulator registers) -- 256-thread
-    // blocks, two vectors per lane, 8 replicas per batch.  Replica loads
-    // stream (nt) in both cases.
-    sh.block = gdt == FC_F16 ? 256 : 64;
+    // Defaults measured best on MI355X: 64-thread blocks, 16 replicas per
+    // batch, streaming (nt) replica loads; one 4-element vector per lane for
+    // fp32 replicas, two for fp16 replicas (half the bytes per load).
+    sh.block = 64;
     sh.vecs = gdt == FC_F16 ? 2 : 1;
-    sh.kchunk = gdt == FC_F16 ? 8 : 16;
+    sh.kchunk = 16;
     sh.nontemporal = 1;
     if (!o) return FC_OK;
     if (o->block_threads) {
@@ -183,7 +181,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     int rc = validate_opts(opts, gdt, sh);
     if (rc) return rc;
 
-    const int vec = gdt == FC_F16 ? 8 : 4;
+    const int vec = 4;
     uint64_t end = 0, n_elems = 0;
     for (int j = 0; j < nseg; ++j) {
         const fc_segment& s = segs[j];

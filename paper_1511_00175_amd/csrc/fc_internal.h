@@ -7,8 +7,8 @@
 
 namespace fc {
 
-// One block's unit of work.  A vector tile covers `count` 16-byte replica
-// vectors (count <= block_threads * vecs_per_thread) starting at element
+// One block's unit of work.  A vector tile covers `count` lane-vectors of 4
+// elements (count <= block_threads * vecs_per_thread) starting at element
 // `start`, all inside segment `seg & SEG_MASK`.  A tail tile (bit TAIL_BIT of
 // `seg` set) covers the last `count` < vector-width elements of a segment
 // whose length is not a multiple of the vector width; its lanes work on one
@@ -29,7 +29,7 @@ struct Shape {
     int dtype;        // fc_dtype
     int tree;         // 1 tree order, 0 linear
     int block;        // threads per block
-    int vecs;         // 16-byte vectors per thread per replica (1 or 2)
+    int vecs;         // 4-element lane-vectors per thread (1 or 2)
     int kchunk;       // replicas loaded per batch (8 or 16)
     int nontemporal;  // non-temporal replica loads
     int maxd;         // depth of the pending-subtree stack (>= bit length of K / kchunk)

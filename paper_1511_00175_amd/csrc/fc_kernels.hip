@@ -5,8 +5,9 @@
 // parameter's weight and velocity are updated in the same pass.  Arithmetic
 // intensity is at most (K + 6) flops per (4K + 16) bytes, far below the ridge
 // point of the vector units, so there are no matrix-core instructions here;
-// the design goals are full 16-byte coalesced loads, many loads in flight per
-// thread, and a summation order that is fixed by construction.
+// the design goals are fully coalesced loads (one 4-element vector per lane:
+// 16 bytes of fp32 or 8 bytes of fp16), many loads in flight per thread, and
+// a summation order that is fixed by construction.
 //
 // Summation order (Sec. 6.2 "Reduction tree", Fig. 3b): leaves are replicas
 // 0..K-1 in order; neighbours are paired level by level and an odd last node
@@ -36,7 +37,8 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u4 __attribute__((ext_vector_type(4)));
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 
 template <int N> constexpr int ilog2() { return N <= 1 ? 0 : 1 + ilog2<N / 2>(); }
 
@@ -115,21 +117,24 @@ template <> struct Rep<FC_F32, 1> {
     __device__ static __forceinline__ void widen(const raw& r, float* x) { x[0] = r; }
 };
 
-// fp16 storage: binary16 -> binary32 is exact for every pattern.
-template <> struct Rep<FC_F16, 8> {
-    typedef u4 raw;
+// fp16 storage: binary16 -> binary32 is exact for every pattern.  A lane
+// takes 4 consecutive fp16 values (8 bytes), so that the lane's fp32 weights,
+// velocity and results are one 16-byte vector and every fp32 store of a wave
+// covers whole cache lines.
+template <> struct Rep<FC_F16, 4> {
+    typedef u2 raw;
     template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
         if constexpr (NT) {
-            return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
-                                                                               CPOL_STREAM_LOAD));
+            return __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), off, 0,
+                                                                              CPOL_STREAM_LOAD));
         } else {
-            return *reinterpret_cast<const FC_GLOBAL u4*>(base + off);
+            return *reinterpret_cast<const FC_GLOBAL u2*>(base + off);
         }
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
-        const h8 h = __builtin_bit_cast(h8, r);
+        const h4 h = __builtin_bit_cast(h4, r);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) x[i] = static_cast<float>(h[i]);
+        for (int i = 0; i < 4; ++i) x[i] = static_cast<float>(h[i]);
     }
 };
 
@@ -503,7 +508,7 @@ template <int A, int B, class F> hipError_t pick(int x, F&& f) {
 
 template <int DT, int TREE, int MODE, int U, int C, int MAXD, int NT>
 hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
-    constexpr int V = DT == FC_F16 ? 8 : 4;
+    constexpr int V = 4;  // elements per lane-vector for both storage types
     hipLaunchKernelGGL((reduce_kernel<DT, V, U, C, MAXD, (TREE != 0), (NT != 0), MODE>), dim3(grid),
                        dim3(block), 0, s, a);
     return hipGetLastError();
@@ -533,20 +538,16 @@ hipError_t launch_reduce(const Shape& sh, int mode, int grid, const ReduceArgs& 
 }
 
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s) {
-    return pick<4, 8>(sh.dtype == FC_F16 ? 8 : 4, [&](auto v) {
-        return pick<1, 2>(sh.vecs, [&](auto u) {
-            hipLaunchKernelGGL((sgd_kernel<v.value, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
-            return hipGetLastError();
-        });
+    return pick<1, 2>(sh.vecs, [&](auto u) {
+        hipLaunchKernelGGL((sgd_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
+        return hipGetLastError();
     });
 }
 
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s) {
-    return pick<4, 8>(sh.dtype == FC_F16 ? 8 : 4, [&](auto v) {
-        return pick<1, 2>(sh.vecs, [&](auto u) {
-            hipLaunchKernelGGL((bcast_kernel<v.value, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
-            return hipGetLastError();
-        });
+    return pick<1, 2>(sh.vecs, [&](auto u) {
+        hipLaunchKernelGGL((bcast_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
+        return hipGetLastError();
     });
 }
 

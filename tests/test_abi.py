@@ -48,7 +48,7 @@ def test_strerror(fcmod):
     ([(0, 16)], 0, 0, None, -1),                       # K < 1
     ([(0, 16)], 1025, 0, None, -1),                    # K > 1024
     ([(2, 16)], 4, 0, None, -2),                       # fp32 offset not a multiple of 4
-    ([(4, 16)], 4, 1, None, -2),                       # fp16 offset not a multiple of 8
+    ([(2, 16)], 4, 1, None, -2),                       # fp16 offset not a multiple of 4
     ([(64, 16), (0, 16)], 4, 0, None, -1),             # unsorted
     ([(0, 16), (8, 16)], 4, 0, None, -1),              # overlapping
     ([(0, 16)], 4, 7, None, -1),                       # bad dtype

@@ -1,0 +1,92 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py
+times (the plan defaults), on sampled outputs the oracle computes one by one.
+
+For each of the five workloads (flat 2^20 x K=4, NiN x K=32, GoogLeNet
+x K=128, VGG-19 x K=16, AlexNet fp16 x K=128) the inputs are drawn on the
+device, two fused steps run on the GPU, and at every segment's first, second,
+last and one random element plus 1500 random elements the oracle recomputes
+the same two steps from the gathered inputs; w' and v' must match bit for bit.
+A property that holds at any size is checked on the whole buffer: the fused
+step equals reduce, then SGD, then (for GoogLeNet) nothing else differs.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_cases import same_bits
+from workloads import gen, tables
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fc(device):
+    import paper_1511_00175_amd as m
+    return m
+
+
+def sample_indices(wl, rng, n_random=1500):
+    """Each segment's first, second, last and one random element, plus
+    n_random elements drawn with probability proportional to segment length."""
+    idx = []
+    for s in wl.segments:
+        idx += [s.offset, s.offset + min(1, s.length - 1), s.offset + s.length - 1,
+                s.offset + int(rng.integers(0, s.length))]
+    lens = np.array([s.length for s in wl.segments], dtype=np.float64)
+    js = rng.choice(len(wl.segments), n_random, p=lens / lens.sum())
+    idx += [wl.segments[j].offset + int(rng.integers(0, wl.segments[j].length)) for j in js]
+    return np.unique(np.array(idx, dtype=np.int64))
+
+
+def segment_of(wl, idx):
+    offs = np.array([s.offset for s in wl.segments])
+    return np.searchsorted(offs, idx, side="right") - 1
+
+
+@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "vgg19", "alexnet"])
+def test_fullsize_sampled(fc, name):
+    import torch
+    wl = tables.get(name)
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(len(name))
+    reps, w, v = gen.device_inputs(wl, 1511, dev)
+    idx = sample_indices(wl, rng)
+    it = torch.from_numpy(idx).to(dev)
+    g_s = reps[:, it].cpu().numpy()                 # (K, S) gathered replica values
+    w_s, v_s = w[it].cpu().numpy(), v[it].cpu().numpy()
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
+    for _ in range(2):
+        plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
+    torch.cuda.synchronize()
+    got_w, got_v = w[it].cpu().numpy(), v[it].cpu().numpy()
+    plan.close()
+    del reps, w, v
+    torch.cuda.empty_cache()
+    # oracle on the gathered samples: each sample is a one-element segment
+    # carrying its own segment's multipliers
+    js = segment_of(wl, idx)
+    rows = [(i, 1, wl.segments[j].lr_mult, wl.segments[j].decay_mult) for i, j in enumerate(js)]
+    ew, ev = w_s, v_s
+    for _ in range(2):
+        ew, ev, _, _ = oracle.step(rows, list(g_s), ew, ev, wl.lr, wl.mu, wl.wd, wl.batch)
+    assert same_bits(got_w, ew) == 0 and same_bits(got_v, ev) == 0
+
+
+def test_fullsize_fused_equals_composed(fc):
+    """At full GoogLeNet size: one fused step == tree reduce, then SGD, on the
+    whole buffer (a property independent of the oracle)."""
+    import torch
+    wl = tables.googlenet()
+    dev = torch.device("cuda:0")
+    reps, w, v = gen.device_inputs(wl, 7, dev)
+    v.normal_(0, 1e-3, generator=torch.Generator(device=dev).manual_seed(8))
+    w2, v2 = w.clone(), v.clone()
+    g = torch.zeros_like(w)
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
+    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
+    plan.tree_reduce(reps, g)
+    plan.sgd_step(w2, v2, g, wl.lr, wl.mu, wl.wd, wl.batch)
+    torch.cuda.synchronize()
+    assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
+    assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
+    plan.close()

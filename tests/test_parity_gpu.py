@@ -24,7 +24,7 @@ def fc(device):
 
 def table(seed, dtype, nseg=9, max_len=5000):
     rng = np.random.default_rng(seed)
-    vec = 8 if dtype == "f16" else 4
+    vec = 4  # offsets: multiples of 4 elements for both storage types
     rows, _ = gen.random_table(rng, nseg, max_len, vec)
     # a tiny segment, one exactly one default tile long, one a tile plus one
     off = rows[-1][0] + rows[-1][1]
