@@ -1,15 +1,17 @@
 #!/usr/bin/env python3
 """Benchmark of the fused tree-reduce + momentum-SGD step on one MI355X.
 
-One step = one fc_step launch over all K synthetic gradient replicas of a
+One step = one fc_step call over all K synthetic gradient replicas of a
 workload (reduce in binary-tree order, average, SGD with momentum and weight
-decay, write back w and v), with every input resident in device memory.
+decay, write back w and v), with every input resident in device memory.  The
+plan's schedule runs the step as one fused kernel or as a reduce pass and an
+update pass (GoogLeNet K=128).
 
 Prints ONE JSON line: effective HBM GB/s of the step (algorithmic bytes per
-step / wall time per step over the timed steps), the kernel's roofline entry
-(algorithmic bytes / average kernel duration from HIP events, against the
-8 TB/s HBM3E peak), and the oracle timed on a bounded sample on one host
-core as a CPU baseline.
+step / wall time per step over the timed steps), the roofline entry of the
+dominant kernel (its algorithmic bytes per launch / its average duration from
+HIP events the library records on the launch stream, against the 8 TB/s HBM3E
+peak), and the oracle timed on one host core as a CPU baseline.
 
     python bench.py [--workload googlenet] [--steps 200] [--warmup 20]
 """
@@ -39,9 +41,27 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary for
-    this workload, or None when absent or taken on another kernel version."""
+def kernel_bytes(wl, kind, out=False, bcast=False):
+    """Algorithmic HBM bytes of one launch of a kernel kind over N parameters:
+    step   : K replicas + w, v read, w', v' written (+ raw sum, + broadcast)
+    reduce : K replicas read, raw sum written
+    sgd    : raw sum, w, v read, w', v' written (+ broadcast)"""
+    n, K, sg = wl.n_params, wl.K, wl.s_g
+    if kind == "step":
+        return n * (K * sg + 16) + (4 * n if out else 0) + (4 * n * K if bcast else 0)
+    if kind == "reduce":
+        return n * (K * sg + 4)
+    if kind == "sgd":
+        return n * 20 + (4 * n * K if bcast else 0)
+    if kind == "bcast":
+        return n * (4 + 4 * K)
+    raise ValueError(kind)
+
+
+def read_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary for this workload, or None when absent or taken on another
+    version of the library sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -51,7 +71,7 @@ def read_traffic(workload):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha256_16") != kernel_hash():
+    if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("kernel") != kernel:
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -138,6 +158,8 @@ def main():
                     help="after the measurement, run a plain device copy of this many MiB three times "
                          "(reference kernel of known size for hardware byte counters)")
     ap.add_argument("--print-hash", action="store_true", help="print the library source hash and exit")
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="do not record per-kernel events (roofline entry then uses the wall time per step)")
     args = ap.parse_args()
 
     if args.print_hash:
@@ -179,17 +201,24 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
-    torch.cuda.synchronize()
+    # timed region 1: the steps alone (barrier = device synchronize on both sides)
     t0 = time.perf_counter()
     for i in range(args.steps):
-        ev[2 * i].record(stream)
         step()
-        ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    durs = [ev[2 * i].elapsed_time(ev[2 * i + 1]) * 1e-3 for i in range(args.steps)]
+    # timed region 2: the same steps with per-kernel HIP events, which the
+    # library records on the launch stream (the current torch stream); the
+    # events add small gaps between kernels, so `value` comes from region 1
+    timing = {}
+    if not args.no_kernel_timing:
+        plan.set_timing(True)
+        plan.read_timing()
+        for i in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        timing = plan.read_timing()
+        plan.set_timing(False)
     for _ in range(args.profile_loop):
         step()
     torch.cuda.synchronize()
@@ -205,10 +234,18 @@ def main():
     bytes_step = wl.algorithmic_bytes(out=args.out, bcast=args.bcast)
     ms_per_step = wall / args.steps * 1e3
     value = bytes_step / (wall / args.steps) / 1e9
-    avg = sum(durs) / len(durs)
-    med = sorted(durs)[len(durs) // 2]
-    achieved = bytes_step / avg / 1e9
-    traffic = read_traffic(wl.name) if not (args.out or args.bcast or args.order != "tree" or opts) else None
+    kernels = {k: {"launches": n, "avg_us": round(us / n, 2),
+                   "algorithmic_bytes": kernel_bytes(wl, k, args.out, bcast=args.bcast and k != "reduce")}
+               for k, (n, us) in timing.items() if n}
+    if not kernels:  # no per-kernel events: the whole step stands in for its kernels
+        kernels = {"step": {"launches": args.steps, "avg_us": round(ms_per_step * 1e3, 2),
+                            "algorithmic_bytes": bytes_step}}
+    dom = max(kernels, key=lambda k: kernels[k]["launches"] * kernels[k]["avg_us"])
+    avg = kernels[dom]["avg_us"] * 1e-6
+    achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
+    plain = not (args.out or args.bcast or args.order != "tree" or opts)
+    traffic = read_traffic(wl.name, dom) if plain else None
+    sched = {1: "fused", 2: "two-pass"}.get(info.schedule, str(info.schedule))
 
     res = {
         "metric": METRIC,
@@ -233,7 +270,8 @@ def main():
             "algorithmic_bytes_per_step": bytes_step,
             "launch": {"grid": info.grid, "tiles": info.ntiles, "block_threads": info.block_threads,
                        "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk,
-                       "nontemporal": info.nontemporal},
+                       "nontemporal": info.nontemporal, "schedule": sched},
+            "kernels": kernels,
             "parallelism": "single GPU",
         },
         "roofline": {
@@ -243,9 +281,10 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": "fc::reduce_kernel (fused step)",
+            "kernel": {"step": "fc::reduce_kernel (fused step)", "reduce": "fc::reduce_kernel (reduce pass)",
+                       "sgd": "fc::sgd_kernel", "bcast": "fc::bcast_kernel"}[dom],
             "kernel_us_avg": round(avg * 1e6, 2),
-            "kernel_us_median": round(med * 1e6, 2),
+            "kernel_algorithmic_bytes": kernels[dom]["algorithmic_bytes"],
         },
         "cpu_baseline": None,
     }

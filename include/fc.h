@@ -83,6 +83,14 @@ typedef enum { FC_ORDER_TREE = 0, FC_ORDER_LINEAR = 1 } fc_order;
 
 typedef struct fc_plan fc_plan;
 
+/* How fc_step schedules the work.  FUSED: one kernel reads the replicas and
+ * w, v and writes w', v'.  TWO_PASS: one kernel reduces into a raw-sum
+ * buffer, a second applies the update (same bits; on MI355X this is faster
+ * when the replicas dominate the bytes, because HBM serves a replica stream
+ * with one write stream better than with two).  AUTO picks TWO_PASS when a
+ * parameter's replicas take more than 256 bytes (K * bytes per element). */
+typedef enum { FC_SCHED_AUTO = 0, FC_SCHED_FUSED = 1, FC_SCHED_TWO_PASS = 2 } fc_schedule;
+
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero (or -1 for `nontemporal`) selects the
  * default. */
@@ -92,13 +100,16 @@ typedef struct {
     int kchunk;          /* replicas loaded per batch: 8 or 16 (default 16) */
     int nontemporal;     /* 1: replica loads carry the streaming (nt) hint (default); 0: plain loads */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
+    int schedule;        /* fc_schedule of fc_step (default FC_SCHED_AUTO) */
 } fc_launch_opts;
 
 /* Create a plan for K workers over a segment table (Sec. 6: one gradient
  * vector per worker).  segs[0..nseg-1] is copied; nseg may be 0 (every call
  * then does nothing).  1 <= K <= 1024.  Offsets must be multiples of 4
  * elements (16 bytes of fp32, 8 bytes of fp16).  Allocates the plan's device
- * tables on the current device with hipMalloc (FC_EHIP on failure).
+ * tables on the current device with hipMalloc (FC_EHIP on failure); when
+ * fc_step's schedule resolves to TWO_PASS the plan also owns a raw-sum
+ * scratch buffer of 4 bytes per element of the segment extent.
  * On success *plan receives the plan; on failure *plan is set to NULL. */
 int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,
                    fc_order order);
@@ -142,7 +153,9 @@ int fc_broadcast(fc_plan* plan, const float* src, float* const* dst, void* strea
  *               may be exactly grads[k] for an FC_F32 plan)
  *   bcast_dst : NULL, or a host array of K device fp32 pointers that
  *               receive w' (the workers' local model copies)
- * Result bits equal fc_tree_reduce, then fc_sgd_step, then fc_broadcast of w.
+ * Result bits equal fc_tree_reduce, then fc_sgd_step, then fc_broadcast of w,
+ * whatever the plan's schedule (in the two-pass schedule `out`, when given,
+ * holds the raw sum between the passes; otherwise the plan's scratch does).
  * w, v, out and every destination must not overlap each other or a replica
  * (FC_EALIAS), except out == grads[k] as above. */
 int fc_step(fc_plan* plan, const void* const* grads, float* w, float* v, float lr, float mu,
@@ -165,9 +178,27 @@ typedef struct {
     int vecs_per_thread;
     int kchunk;
     int nontemporal;
+    int schedule;        /* resolved fc_schedule of fc_step: FUSED or TWO_PASS */
+    uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
 } fc_plan_info;
 
 int fc_plan_query(const fc_plan* plan, fc_plan_info* info);
+
+/* Per-kernel timing, for benchmarks and tracing.  While enabled, every kernel
+ * the plan launches is bracketed by two HIP events recorded on the launch
+ * stream.  fc_plan_read_timing waits for the recorded events, returns per
+ * kernel kind the number of launches and their summed duration (us) since
+ * the previous read, and clears the record.  Enabling adds two event records
+ * per launch and nothing else. */
+enum { FC_KERNEL_STEP = 0, FC_KERNEL_REDUCE = 1, FC_KERNEL_SGD = 2, FC_KERNEL_BCAST = 3, FC_KERNEL_KINDS = 4 };
+
+typedef struct {
+    int launches[FC_KERNEL_KINDS];
+    double total_us[FC_KERNEL_KINDS];
+} fc_timing;
+
+int fc_plan_set_timing(fc_plan* plan, int enable);
+int fc_plan_read_timing(fc_plan* plan, fc_timing* timing);
 
 #ifdef __cplusplus
 }

@@ -9,12 +9,12 @@ The work is done by HIP kernels behind the C ABI of include/fc.h; this package
 only marshals torch tensors (device memory and the current stream) into it.
 """
 from . import _fc
-from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FcError,  # noqa: F401
-                  fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query, fc_sgd_step, fc_step,
-                  fc_strerror, fc_tree_reduce)
+from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
+                  FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
+                  fc_plan_read_timing, fc_plan_set_timing, fc_sgd_step, fc_step, fc_strerror, fc_tree_reduce)
 
-__all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_tree_reduce",
-           "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror"]
+__all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
+           "fc_plan_read_timing", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror"]
 
 _DTYPES = {"f32": FC_F32, "f16": FC_F16}
 _ORDERS = {"tree": FC_ORDER_TREE, "linear": FC_ORDER_LINEAR}
@@ -49,7 +49,8 @@ class Plan:
     dtype   : replica storage, "f32" or "f16".
     order   : "tree" (reduction tree) or "linear" (parameter server).
     opts    : launch shape (block_threads, vecs_per_thread, kchunk,
-              nontemporal, max_blocks); results do not depend on it.
+              nontemporal, max_blocks) and fc_step schedule (0 auto,
+              1 fused, 2 two-pass); results do not depend on them.
     """
 
     def __init__(self, segments, K, dtype="f32", order="tree", **opts):
@@ -74,6 +75,15 @@ class Plan:
 
     def info(self):
         return fc_plan_query(self.handle)
+
+    def set_timing(self, enable=True):
+        rc = fc_plan_set_timing(self.handle, enable)
+        if rc:
+            raise FcError("fc_plan_set_timing", rc)
+
+    def read_timing(self):
+        """{kernel: (launches, total us)} since the previous read."""
+        return fc_plan_read_timing(self.handle)
 
     def tree_reduce(self, grads, out, stream=None):
         rc = fc_tree_reduce(self.handle, _rows(grads), _ptr(out), _stream(stream))

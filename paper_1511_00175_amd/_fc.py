@@ -23,14 +23,24 @@ class fc_segment(ctypes.Structure):
 
 class fc_launch_opts(ctypes.Structure):
     _fields_ = [("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int), ("kchunk", ctypes.c_int),
-                ("nontemporal", ctypes.c_int), ("max_blocks", ctypes.c_int)]
+                ("nontemporal", ctypes.c_int), ("max_blocks", ctypes.c_int), ("schedule", ctypes.c_int)]
 
 
 class fc_plan_info(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int), ("nseg", ctypes.c_int), ("dtype", ctypes.c_int), ("order", ctypes.c_int),
                 ("n_elems", ctypes.c_uint64), ("extent", ctypes.c_uint64), ("ntiles", ctypes.c_int),
                 ("grid", ctypes.c_int), ("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int),
-                ("kchunk", ctypes.c_int), ("nontemporal", ctypes.c_int)]
+                ("kchunk", ctypes.c_int), ("nontemporal", ctypes.c_int), ("schedule", ctypes.c_int),
+                ("scratch_bytes", ctypes.c_uint64)]
+
+
+FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS = 0, 1, 2
+FC_KERNEL_STEP, FC_KERNEL_REDUCE, FC_KERNEL_SGD, FC_KERNEL_BCAST, FC_KERNEL_KINDS = 0, 1, 2, 3, 4
+KERNEL_NAMES = ("step", "reduce", "sgd", "bcast")
+
+
+class fc_timing(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int * FC_KERNEL_KINDS), ("total_us", ctypes.c_double * FC_KERNEL_KINDS)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -56,8 +66,10 @@ lib.fc_step.argtypes = [_plan_p, _pp, _vp, _vp, _f, _f, _f, _i, _vp, _pp, _vp]
 lib.fc_strerror.argtypes = [_i]
 lib.fc_strerror.restype = ctypes.c_char_p
 lib.fc_plan_query.argtypes = [_plan_p, ctypes.POINTER(fc_plan_info)]
+lib.fc_plan_set_timing.argtypes = [_plan_p, _i]
+lib.fc_plan_read_timing.argtypes = [_plan_p, ctypes.POINTER(fc_timing)]
 for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
-           "fc_plan_query"):
+           "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing"):
     getattr(lib, _n).restype = ctypes.c_int
 
 
@@ -101,7 +113,7 @@ def fc_plan_create(segs, K, gdt=FC_F32, order=FC_ORDER_TREE, opts=None):
     if opts is None:
         rc = lib.fc_plan_create(ctypes.byref(h), arr, n, int(K), int(gdt), int(order))
     else:
-        o = fc_launch_opts(0, 0, 0, -1, 0)
+        o = fc_launch_opts(0, 0, 0, -1, 0, 0)
         for k, v in opts.items():
             setattr(o, k, int(v))
         rc = lib.fc_plan_create_ex(ctypes.byref(h), arr, n, int(K), int(gdt), int(order), ctypes.byref(o))
@@ -116,6 +128,17 @@ def fc_plan_query(plan):
     info = fc_plan_info()
     _check("fc_plan_query", lib.fc_plan_query(plan, ctypes.byref(info)))
     return info
+
+
+def fc_plan_set_timing(plan, enable):
+    return lib.fc_plan_set_timing(plan, 1 if enable else 0)
+
+
+def fc_plan_read_timing(plan):
+    """{kernel name: (launches, total us)} since the previous read."""
+    t = fc_timing()
+    _check("fc_plan_read_timing", lib.fc_plan_read_timing(plan, ctypes.byref(t)))
+    return {KERNEL_NAMES[i]: (t.launches[i], t.total_us[i]) for i in range(FC_KERNEL_KINDS)}
 
 
 def fc_tree_reduce(plan, grads, out, stream=0):

@@ -33,6 +33,17 @@ struct fc_plan {
     float* d_mults = nullptr;
     const void** d_grads = nullptr;  // K replica pointers
     float** d_dst = nullptr;         // K broadcast pointers
+    float* d_sum = nullptr;          // raw-sum scratch of the two-pass schedule (extent floats)
+    int schedule = FC_SCHED_FUSED;   // resolved schedule of fc_step
+
+    // per-kernel timing (fc_plan_set_timing / fc_plan_read_timing)
+    struct Rec {
+        hipEvent_t a, b;
+        int kind;
+    };
+    bool timing = false;
+    std::vector<hipEvent_t> event_pool;
+    std::vector<Rec> records;
 
     // host copies of what the device pointer tables hold (valid flags)
     std::vector<const void*> h_grads;
@@ -132,6 +143,7 @@ int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc::Shape& sh) {
         sh.nontemporal = o->nontemporal;
     }
     if (o->max_blocks < 0) return FC_EINVAL;
+    if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_TWO_PASS) return FC_EINVAL;
     return FC_OK;
 }
 
@@ -146,11 +158,59 @@ int bit_length(int x) {
 
 void free_plan(fc_plan* p) {
     if (!p) return;
+    for (auto& r : p->records) {
+        (void)hipEventDestroy(r.a);
+        (void)hipEventDestroy(r.b);
+    }
+    for (auto e : p->event_pool) (void)hipEventDestroy(e);
+    if (p->d_sum) (void)hipFree(p->d_sum);
     if (p->d_tiles) (void)hipFree(p->d_tiles);
     if (p->d_mults) (void)hipFree(p->d_mults);
     if (p->d_grads) (void)hipFree(p->d_grads);
     if (p->d_dst) (void)hipFree(p->d_dst);
     delete p;
+}
+
+hipError_t take_event(fc_plan* p, hipEvent_t* e) {
+    if (!p->event_pool.empty()) {
+        *e = p->event_pool.back();
+        p->event_pool.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(e);
+}
+
+// Launch `go` on stream s; with timing on, bracket it with two events.
+template <typename F>
+int launch(fc_plan* p, int kind, hipStream_t s, F&& go) {
+    if (!p->timing) return hip_rc(go());
+    fc_plan::Rec r{nullptr, nullptr, kind};
+    if (take_event(p, &r.a) != hipSuccess) return FC_EHIP;
+    if (take_event(p, &r.b) != hipSuccess) {
+        p->event_pool.push_back(r.a);
+        return FC_EHIP;
+    }
+    try {
+        p->records.reserve(p->records.size() + 1);
+    } catch (const std::bad_alloc&) {
+        p->event_pool.push_back(r.a);
+        p->event_pool.push_back(r.b);
+        return FC_ENOMEM;
+    }
+    if (hipEventRecord(r.a, s) != hipSuccess) {
+        p->event_pool.push_back(r.a);
+        p->event_pool.push_back(r.b);
+        return FC_EHIP;
+    }
+    const int rc = hip_rc(go());
+    if (hipEventRecord(r.b, s) != hipSuccess) {
+        // the start event may still complete; both go back to the pool unused
+        p->event_pool.push_back(r.a);
+        p->event_pool.push_back(r.b);
+        return FC_EHIP;
+    }
+    p->records.push_back(r);
+    return rc;
 }
 
 }  // namespace
@@ -257,6 +317,13 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     if (opts && opts->max_blocks > 0) grid = std::min(grid, opts->max_blocks);
     p->grid = grid;
 
+    // fc_step schedule: two passes when the replicas dominate the bytes (see fc_schedule)
+    const int sched = opts ? opts->schedule : FC_SCHED_AUTO;
+    if (sched == FC_SCHED_AUTO)
+        p->schedule = (static_cast<int64_t>(K) * p->sg > 256) ? FC_SCHED_TWO_PASS : FC_SCHED_FUSED;
+    else
+        p->schedule = sched;
+
     if (hipGetDevice(&p->device) != hipSuccess) {
         delete p;
         return FC_EHIP;
@@ -265,6 +332,8 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
               hipMalloc(&p->d_mults, mults.size() * sizeof(float)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_grads), K * sizeof(void*)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_dst), K * sizeof(float*)) == hipSuccess;
+    if (ok && p->schedule == FC_SCHED_TWO_PASS && p->extent > 0)
+        ok = hipMalloc(&p->d_sum, static_cast<size_t>(p->extent) * sizeof(float)) == hipSuccess;
     if (ok && !tiles.empty())
         ok = hipMemcpy(p->d_tiles, tiles.data(), tiles.size() * sizeof(Tile), hipMemcpyHostToDevice) == hipSuccess;
     if (ok)
@@ -298,7 +367,34 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->vecs_per_thread = p->shape.vecs;
     info->kchunk = p->shape.kchunk;
     info->nontemporal = p->shape.nontemporal;
+    info->schedule = p->schedule;
+    info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
     return FC_OK;
+}
+
+int fc_plan_set_timing(fc_plan* p, int enable) {
+    if (!p) return FC_EINVAL;
+    p->timing = enable != 0;
+    return FC_OK;
+}
+
+int fc_plan_read_timing(fc_plan* p, fc_timing* t) {
+    if (!p || !t) return FC_EINVAL;
+    std::memset(t, 0, sizeof(*t));
+    int rc = FC_OK;
+    for (auto& r : p->records) {
+        float ms = 0.0f;
+        if (rc == FC_OK && (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess))
+            rc = FC_EHIP;
+        if (rc == FC_OK) {
+            t->launches[r.kind] += 1;
+            t->total_us[r.kind] += 1e3 * static_cast<double>(ms);
+        }
+        p->event_pool.push_back(r.a);
+        p->event_pool.push_back(r.b);
+    }
+    p->records.clear();
+    return rc;
 }
 
 namespace {
@@ -352,7 +448,7 @@ int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* strea
     a.grads = p->d_grads;
     a.K = p->K;
     a.out = out;
-    rc = hip_rc(fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s));
+    rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }
@@ -378,7 +474,7 @@ int fc_sgd_step(fc_plan* p, float* w, float* v, const float* g, float lr, float 
     a.mu = mu;
     a.wd = wd;
     a.c = 1.0f / static_cast<float>(batch);
-    rc = hip_rc(fc::launch_sgd(p->shape, p->grid, a, s));
+    rc = launch(p, FC_KERNEL_SGD, s, [&] { return fc::launch_sgd(p->shape, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }
@@ -401,7 +497,7 @@ int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) 
     a.src = src;
     a.dst = p->d_dst;
     a.K = p->K;
-    rc = hip_rc(fc::launch_bcast(p->shape, p->grid, a, s));
+    rc = launch(p, FC_KERNEL_BCAST, s, [&] { return fc::launch_bcast(p->shape, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }
@@ -430,6 +526,37 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
         rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, bcast_dst, s);
         if (rc) return rc;
     }
+    const float c = 1.0f / static_cast<float>(batch);
+    if (p->schedule == FC_SCHED_TWO_PASS) {
+        // pass 1: raw sum into `out` (or the plan's scratch); pass 2: update (+ broadcast)
+        float* sum = out ? out : p->d_sum;
+        fc::ReduceArgs r{};
+        r.tiles = p->d_tiles;
+        r.ntiles = p->ntiles;
+        r.mults = p->d_mults;
+        r.grads = p->d_grads;
+        r.K = p->K;
+        r.out = sum;
+        rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, r, s); });
+        if (rc == FC_OK) {
+            fc::SgdArgs g{};
+            g.tiles = p->d_tiles;
+            g.ntiles = p->ntiles;
+            g.mults = p->d_mults;
+            g.w = w;
+            g.v = v;
+            g.g = sum;
+            g.dst = bcast_dst ? p->d_dst : nullptr;
+            g.K = p->K;
+            g.lr = lr;
+            g.mu = mu;
+            g.wd = wd;
+            g.c = c;
+            rc = launch(p, FC_KERNEL_SGD, s, [&] { return fc::launch_sgd(p->shape, p->grid, g, s); });
+        }
+        note_stream(p, s);
+        return rc;
+    }
     fc::ReduceArgs a{};
     a.tiles = p->d_tiles;
     a.ntiles = p->ntiles;
@@ -443,8 +570,8 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     a.lr = lr;
     a.mu = mu;
     a.wd = wd;
-    a.c = 1.0f / static_cast<float>(batch);
-    rc = hip_rc(fc::launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s));
+    a.c = c;
+    rc = launch(p, FC_KERNEL_STEP, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }

@@ -55,6 +55,8 @@ struct SgdArgs {
     float* w;
     float* v;
     const float* g;
+    float* const* dst;            // device table of K broadcast pointers, or nullptr
+    int K;
     float lr, mu, wd, c;
 };
 

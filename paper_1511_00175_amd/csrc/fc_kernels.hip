@@ -458,6 +458,8 @@ __device__ __forceinline__ void sgd_body(const SgdArgs& a, uint64_t start, uint3
         for (int i = 0; i < V; ++i) sgd1(g[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
         st32r<V>(gwrite(a.w) + start4, off, wn);
         st32r<V>(gwrite(a.v) + start4, off, vn);
+        if (a.dst)
+            for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
     }
 }
 

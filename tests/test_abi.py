@@ -25,7 +25,8 @@ def fcmod():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("fc_plan_create", "fc_plan_create_ex", "fc_plan_destroy", "fc_tree_reduce", "fc_sgd_step",
-              "fc_broadcast", "fc_step", "fc_strerror", "fc_plan_query"):
+              "fc_broadcast", "fc_step", "fc_strerror", "fc_plan_query", "fc_plan_set_timing",
+              "fc_plan_read_timing"):
         assert n in names
 
 
@@ -57,6 +58,7 @@ def test_strerror(fcmod):
     ([(0, 16)], 4, 0, {"kchunk": 4}, -1),
     ([(0, 16)], 4, 0, {"nontemporal": 2}, -1),
     ([(0, 16)], 4, 0, {"max_blocks": -1}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 3}, -1),
 ])
 def test_plan_argument_errors(fcmod, segs, K, gdt, opts, code):
     rc, h = fcmod._fc.fc_plan_create(segs, K, gdt, 0, opts)
@@ -71,6 +73,8 @@ def test_null_arguments(fcmod):
     assert f.fc_broadcast(None, 0, [0]) == f.FC_EINVAL
     assert f.fc_step(None, [0], 0, 0, 0.1, 0.9, 0.0, 1) == f.FC_EINVAL
     assert f.lib.fc_plan_query(None, None) == f.FC_EINVAL
+    assert f.lib.fc_plan_set_timing(None, 1) == f.FC_EINVAL
+    assert f.lib.fc_plan_read_timing(None, None) == f.FC_EINVAL
     f.fc_plan_destroy(None)
 
 

@@ -101,6 +101,7 @@ def test_fp16_widening_exhaustive(fc):
 
 SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c, nontemporal=nt)
           for b in (64, 128, 256) for u in (1, 2) for c in (8, 16) for nt in (0, 1)]
+SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, max_blocks=5)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -117,6 +118,55 @@ def test_launch_shape_invariance(fc, dtype):
             ref = got
         assert same_bits(got, ref) == 0
         assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(6), steps=1, opts=opts) == 0, opts
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("schedule", [1, 2])
+@pytest.mark.parametrize("K", [3, 64, 130])
+def test_schedules_match_oracle(fc, K, schedule, dtype):
+    """fc_step in one fused pass and in two passes (raw sum, then update),
+    with and without the raw sum and the broadcast, over chained steps."""
+    segs = table(9000 + K, dtype, nseg=5, max_len=3000)
+    rng = np.random.default_rng(K + schedule)
+    for with_out, with_bcast in ((False, False), (True, False), (False, True), (True, True)):
+        assert run_steps(fc, segs, K, dtype, "tree", rng, steps=2, opts=dict(schedule=schedule),
+                         with_out=with_out, with_bcast=with_bcast) == 0, (with_out, with_bcast)
+
+
+def test_schedule_resolution(fc):
+    """AUTO takes two passes when a parameter's replicas exceed 256 bytes;
+    only then does the plan own a raw-sum scratch buffer."""
+    segs = [(0, 1000, 1, 1), (1024, 5, 1, 1)]
+    for K, dtype, two in ((64, "f32", False), (65, "f32", True), (128, "f16", False), (129, "f16", True)):
+        info = fc.Plan(segs, K, dtype, "tree").info()
+        assert info.schedule == (2 if two else 1), (K, dtype)
+        assert info.scratch_bytes == (4 * 1029 if two else 0)
+    assert fc.Plan(segs, 128, "f32", "tree", schedule=1).info().scratch_bytes == 0
+
+
+def test_timing_records_every_launch(fc):
+    import torch
+    segs = [(0, 5000, 1, 1)]
+    K = 130
+    reps = torch.randn((K, 5120), device="cuda")
+    w, v, g = (torch.zeros(5120, device="cuda") for _ in range(3))
+    for schedule in (1, 2):
+        plan = fc.Plan(segs, K, "f32", "tree", schedule=schedule)
+        plan.set_timing(True)
+        for _ in range(3):
+            plan.step(reps, w, v, 0.1, 0.9, 0.0, 64)
+        plan.tree_reduce(reps, g)
+        t = plan.read_timing()
+        if schedule == 1:
+            assert t["step"][0] == 3 and t["reduce"][0] == 1 and t["sgd"][0] == 0
+        else:
+            assert t["step"][0] == 0 and t["reduce"][0] == 4 and t["sgd"][0] == 3
+        assert all(us > 0 for n, us in t.values() if n)
+        assert all(n == 0 for n, _ in plan.read_timing().values())
+        plan.set_timing(False)
+        plan.step(reps, w, v, 0.1, 0.9, 0.0, 64)
+        assert all(n == 0 for n, _ in plan.read_timing().values())
+        plan.close()
 
 
 def test_fused_equals_composed(fc):
