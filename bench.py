@@ -269,8 +269,7 @@ def main():
             "write_sum": args.out, "broadcast": args.bcast,
             "algorithmic_bytes_per_step": bytes_step,
             "launch": {"grid": info.grid, "tiles": info.ntiles, "block_threads": info.block_threads,
-                       "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk,
-                       "nontemporal": info.nontemporal, "schedule": sched},
+                       "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "schedule": sched},
             "kernels": kernels,
             "parallelism": "single GPU",
         },

@@ -92,13 +92,15 @@ typedef struct fc_plan fc_plan;
 typedef enum { FC_SCHED_AUTO = 0, FC_SCHED_FUSED = 1, FC_SCHED_TWO_PASS = 2 } fc_schedule;
 
 /* Launch shape.  Results are bit-identical for every allowed setting; the
- * fields only change speed.  Zero (or -1 for `nontemporal`) selects the
- * default. */
+ * fields only change speed.  Zero selects the default, which depends on the
+ * replica type and K (measured on MI355X): fp16 -> (4 vectors, 4 replicas,
+ * 256 threads); fp32 with 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16,
+ * 64).  Replica loads always carry the streaming (nt) hint. */
 typedef struct {
-    int block_threads;   /* 64, 128 or 256 threads per block (default 64) */
-    int vecs_per_thread; /* 4-element lane-vectors per thread: 1 or 2 (default 1 fp32, 2 fp16) */
-    int kchunk;          /* replicas loaded per batch: 8 or 16 (default 16) */
-    int nontemporal;     /* 1: replica loads carry the streaming (nt) hint (default); 0: plain loads */
+    int block_threads;   /* 64, 128 or 256 threads per block */
+    int vecs_per_thread; /* 4-element lane-vectors per thread (1, 2 or 4) ... */
+    int kchunk;          /* ... and replicas loaded per batch; the pairs compiled are
+                            (1, 8) (1, 16) (2, 8) (2, 16) (4, 2) (4, 4) (4, 8) */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
     int schedule;        /* fc_schedule of fc_step (default FC_SCHED_AUTO) */
 } fc_launch_opts;
@@ -177,7 +179,6 @@ typedef struct {
     int block_threads;
     int vecs_per_thread;
     int kchunk;
-    int nontemporal;
     int schedule;        /* resolved fc_schedule of fc_step: FUSED or TWO_PASS */
     uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
 } fc_plan_info;

@@ -49,8 +49,8 @@ class Plan:
     dtype   : replica storage, "f32" or "f16".
     order   : "tree" (reduction tree) or "linear" (parameter server).
     opts    : launch shape (block_threads, vecs_per_thread, kchunk,
-              nontemporal, max_blocks) and fc_step schedule (0 auto,
-              1 fused, 2 two-pass); results do not depend on them.
+              max_blocks) and fc_step schedule (0 auto, 1 fused,
+              2 two-pass); results do not depend on them.
     """
 
     def __init__(self, segments, K, dtype="f32", order="tree", **opts):

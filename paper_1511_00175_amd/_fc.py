@@ -23,14 +23,14 @@ class fc_segment(ctypes.Structure):
 
 class fc_launch_opts(ctypes.Structure):
     _fields_ = [("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int), ("kchunk", ctypes.c_int),
-                ("nontemporal", ctypes.c_int), ("max_blocks", ctypes.c_int), ("schedule", ctypes.c_int)]
+                ("max_blocks", ctypes.c_int), ("schedule", ctypes.c_int)]
 
 
 class fc_plan_info(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int), ("nseg", ctypes.c_int), ("dtype", ctypes.c_int), ("order", ctypes.c_int),
                 ("n_elems", ctypes.c_uint64), ("extent", ctypes.c_uint64), ("ntiles", ctypes.c_int),
                 ("grid", ctypes.c_int), ("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int),
-                ("kchunk", ctypes.c_int), ("nontemporal", ctypes.c_int), ("schedule", ctypes.c_int),
+                ("kchunk", ctypes.c_int), ("schedule", ctypes.c_int),
                 ("scratch_bytes", ctypes.c_uint64)]
 
 
@@ -113,7 +113,7 @@ def fc_plan_create(segs, K, gdt=FC_F32, order=FC_ORDER_TREE, opts=None):
     if opts is None:
         rc = lib.fc_plan_create(ctypes.byref(h), arr, n, int(K), int(gdt), int(order))
     else:
-        o = fc_launch_opts(0, 0, 0, -1, 0, 0)
+        o = fc_launch_opts(0, 0, 0, 0, 0)
         for k, v in opts.items():
             setattr(o, k, int(v))
         rc = lib.fc_plan_create_ex(ctypes.byref(h), arr, n, int(K), int(gdt), int(order), ctypes.byref(o))

@@ -112,35 +112,51 @@ int update_table(fc_plan* p, std::vector<P>& host, bool& valid, P* dev, const P*
     return FC_OK;
 }
 
+hipError_t launch_reduce(const fc::Shape& sh, int mode, int grid, const fc::ReduceArgs& a, hipStream_t s) {
+    return sh.dtype == FC_F16 ? fc::launch_reduce_f16(sh, mode, grid, a, s) : fc::launch_reduce_f32(sh, mode, grid, a, s);
+}
+
 void note_stream(fc_plan* p, hipStream_t s) {
     p->last_stream = s;
     p->have_last_stream = true;
 }
 
-int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc::Shape& sh) {
-    // Defaults measured best on MI355X: 64-thread blocks, 16 replicas per
-    // batch, streaming (nt) replica loads; one 4-element vector per lane for
-    // fp32 replicas, two for fp16 replicas (half the bytes per load).
-    sh.block = 64;
-    sh.vecs = gdt == FC_F16 ? 2 : 1;
-    sh.kchunk = 16;
-    sh.nontemporal = 1;
+// Launch-shape defaults, measured on MI355X for the five workloads:
+//   fp16 replicas       : 4 vectors per lane, 4 replicas per batch, 256 threads
+//   fp32, 16 < K <= 64  : 4 vectors per lane, 2 replicas per batch, 256 threads
+//   other fp32          : 1 vector per lane, 16 replicas per batch, 64 threads
+// Four vectors per lane make every wave read 4 KiB of one replica at a time,
+// which HBM serves better than 1 KiB pieces, as long as the lane's registers
+// (16 accumulators per pending subtree) still allow enough waves in flight.
+void default_shape(fc_dtype gdt, int K, fc::Shape& sh) {
+    if (gdt == FC_F16) {
+        sh.vecs = 4; sh.kchunk = 4; sh.block = 256;
+    } else if (K > 16 && K <= 64) {
+        sh.vecs = 4; sh.kchunk = 2; sh.block = 256;
+    } else {
+        sh.vecs = 1; sh.kchunk = 16; sh.block = 64;
+    }
+}
+
+bool compiled_pair(int u, int c) {
+    return (u == 1 && (c == 8 || c == 16)) || (u == 2 && (c == 8 || c == 16)) ||
+           (u == 4 && (c == 2 || c == 4 || c == 8));
+}
+
+int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh) {
+    default_shape(gdt, K, sh);
     if (!o) return FC_OK;
     if (o->block_threads) {
         if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
         sh.block = o->block_threads;
     }
-    if (o->vecs_per_thread) {
-        if (o->vecs_per_thread != 1 && o->vecs_per_thread != 2) return FC_EINVAL;
-        sh.vecs = o->vecs_per_thread;
-    }
-    if (o->kchunk) {
-        if (o->kchunk != 8 && o->kchunk != 16) return FC_EINVAL;
-        sh.kchunk = o->kchunk;
-    }
-    if (o->nontemporal != -1) {
-        if (o->nontemporal != 0 && o->nontemporal != 1) return FC_EINVAL;
-        sh.nontemporal = o->nontemporal;
+    if (o->vecs_per_thread || o->kchunk) {
+        // an explicit pair replaces the default pair; one field alone keeps the other default
+        const int u = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
+        const int c = o->kchunk ? o->kchunk : sh.kchunk;
+        if (!compiled_pair(u, c)) return FC_EINVAL;
+        sh.vecs = u;
+        sh.kchunk = c;
     }
     if (o->max_blocks < 0) return FC_EINVAL;
     if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_TWO_PASS) return FC_EINVAL;
@@ -238,7 +254,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     if (gdt != FC_F32 && gdt != FC_F16) return FC_EINVAL;
     if (order != FC_ORDER_TREE && order != FC_ORDER_LINEAR) return FC_EINVAL;
     fc::Shape sh{};
-    int rc = validate_opts(opts, gdt, sh);
+    int rc = validate_opts(opts, gdt, K, sh);
     if (rc) return rc;
 
     const int vec = 4;
@@ -266,11 +282,11 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     sh.dtype = gdt;
     sh.tree = order == FC_ORDER_TREE;
     const int need = bit_length(K / sh.kchunk);
-    if (need > fc::MAXD_LARGE) {
+    if (need > fc::MAXD_MAX) {
         delete p;
         return FC_EINVAL;
     }
-    sh.maxd = need <= fc::MAXD_SMALL ? fc::MAXD_SMALL : fc::MAXD_LARGE;
+    sh.maxd = need;
     p->shape = sh;
 
     // Tile map: each segment is cut into tiles of at most block*vecs vectors;
@@ -366,7 +382,6 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->block_threads = p->shape.block;
     info->vecs_per_thread = p->shape.vecs;
     info->kchunk = p->shape.kchunk;
-    info->nontemporal = p->shape.nontemporal;
     info->schedule = p->schedule;
     info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
     return FC_OK;
@@ -448,7 +463,7 @@ int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* strea
     a.grads = p->d_grads;
     a.K = p->K;
     a.out = out;
-    rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s); });
+    rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }
@@ -537,7 +552,7 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
         r.grads = p->d_grads;
         r.K = p->K;
         r.out = sum;
-        rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, r, s); });
+        rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, r, s); });
         if (rc == FC_OK) {
             fc::SgdArgs g{};
             g.tiles = p->d_tiles;
@@ -571,7 +586,7 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     a.mu = mu;
     a.wd = wd;
     a.c = c;
-    rc = launch(p, FC_KERNEL_STEP, s, [&] { return fc::launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
+    rc = launch(p, FC_KERNEL_STEP, s, [&] { return launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
     note_stream(p, s);
     return rc;
 }

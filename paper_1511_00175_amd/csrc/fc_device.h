@@ -1,4 +1,6 @@
-// Kernels of the gradient-aggregation + SGD step for gfx950 (CDNA4).
+// Device code of the gradient-aggregation + SGD step for gfx950 (CDNA4),
+// included by the translation units that instantiate the kernels
+// (fc_reduce_f32.hip, fc_reduce_f16.hip, fc_update.hip).
 //
 // The work is a bandwidth-bound reduction: every element of every replica is
 // read once, the K values of one parameter are added in registers, and the
@@ -25,6 +27,8 @@
 //   ga = s*c ; d = ga + wd_j*w ; v' = mu*v + lr_j*d ; w' = w - v'
 // Every operation is one rounded fp32 op: contraction is disabled below and
 // the library is built with -ffp-contract=off.
+#pragma once
+
 #include <type_traits>
 
 #include "fc.h"
@@ -94,13 +98,9 @@ template <int DT, int V> struct Rep;
 // element (uniform), `off` the lane's byte offset inside the tile.
 template <> struct Rep<FC_F32, 4> {
     typedef f4 raw;
-    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        if constexpr (NT) {
-            return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
-                                                                               CPOL_STREAM_LOAD));
-        } else {
-            return *reinterpret_cast<const FC_GLOBAL f4*>(base + off);
-        }
+    __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
+                                                                           CPOL_STREAM_LOAD));
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
         x[0] = r.x; x[1] = r.y; x[2] = r.z; x[3] = r.w;
@@ -109,10 +109,8 @@ template <> struct Rep<FC_F32, 4> {
 
 template <> struct Rep<FC_F32, 1> {
     typedef float raw;
-    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        const FC_GLOBAL float* q = reinterpret_cast<const FC_GLOBAL float*>(base + off);
-        if constexpr (NT) return __builtin_nontemporal_load(q);
-        else return *q;
+    __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        return *reinterpret_cast<const FC_GLOBAL float*>(base + off);
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) { x[0] = r; }
 };
@@ -123,13 +121,9 @@ template <> struct Rep<FC_F32, 1> {
 // covers whole cache lines.
 template <> struct Rep<FC_F16, 4> {
     typedef u2 raw;
-    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        if constexpr (NT) {
-            return __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), off, 0,
-                                                                              CPOL_STREAM_LOAD));
-        } else {
-            return *reinterpret_cast<const FC_GLOBAL u2*>(base + off);
-        }
+    __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        return __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), off, 0,
+                                                                          CPOL_STREAM_LOAD));
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
         const h4 h = __builtin_bit_cast(h4, r);
@@ -140,10 +134,8 @@ template <> struct Rep<FC_F16, 4> {
 
 template <> struct Rep<FC_F16, 1> {
     typedef unsigned short raw;
-    template <bool NT> __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
-        const FC_GLOBAL unsigned short* q = reinterpret_cast<const FC_GLOBAL unsigned short*>(base + off);
-        if constexpr (NT) return __builtin_nontemporal_load(q);
-        else return *q;
+    __device__ static __forceinline__ raw load(gptr_t base, uint32_t off) {
+        return *reinterpret_cast<const FC_GLOBAL unsigned short*>(base + off);
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) {
         x[0] = static_cast<float>(__builtin_bit_cast(_Float16, r));
@@ -216,12 +208,12 @@ template <int U, int V> __device__ __forceinline__ void add_right(Acc<U, V>& d, 
 
 // Replica k's vectors of this lane: the replica pointer comes from the plan's
 // table (scalar load), the tile start is added in scalar registers.
-template <int DT, int V, int U, bool NT>
+template <int DT, int V, int U>
 __device__ __forceinline__ void load_leaf(const void* const* grads, int k, uint64_t start_bytes,
                                           const uint32_t (&off)[U], typename Rep<DT, V>::raw (&r)[U]) {
     const gptr_t base = gread(ldc(grads, k)) + start_bytes;
 #pragma unroll
-    for (int u = 0; u < U; ++u) r[u] = Rep<DT, V>::template load<NT>(base, off[u]);
+    for (int u = 0; u < U; ++u) r[u] = Rep<DT, V>::load(base, off[u]);
 }
 
 template <int DT, int V, int U>
@@ -273,7 +265,7 @@ __device__ __forceinline__ void fold(const Acc<U, V> (&st)[D], int n, Acc<U, V>&
 }
 
 // Sum over the K replicas of V elements at e[u], u < U, in tree or linear order.
-template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT>
+template <int DT, int V, int U, int C, int MAXD, bool TREE>
 __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t start_bytes,
                                        const uint32_t (&off)[U], Acc<U, V>& acc) {
     typedef typename Rep<DT, V>::raw raw_t;
@@ -286,7 +278,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
         for (int c = 0; c < nfull; ++c) {
             raw_t raw[C][U];
 #pragma unroll
-            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, NT>(grads, c * C + j, start_bytes, off, raw[j]);
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U>(grads, c * C + j, start_bytes, off, raw[j]);
             Acc<U, V> x[C];
 #pragma unroll
             for (int j = 0; j < C; ++j) widen_leaf<DT, V, U>(x[j], raw[j]);
@@ -306,7 +298,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
             raw_t raw[C - 1][U];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i)
-                if (i < r) load_leaf<DT, V, U, NT>(grads, nfull * C + i, start_bytes, off, raw[i]);
+                if (i < r) load_leaf<DT, V, U>(grads, nfull * C + i, start_bytes, off, raw[i]);
             Acc<U, V> rs[LC];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i) {
@@ -324,7 +316,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
         for (int c = 0; c < nfull; ++c) {
             raw_t raw[C][U];
 #pragma unroll
-            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, NT>(grads, c * C + j, start_bytes, off, raw[j]);
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U>(grads, c * C + j, start_bytes, off, raw[j]);
 #pragma unroll
             for (int j = 0; j < C; ++j) {
                 Acc<U, V> x;
@@ -338,7 +330,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
             raw_t raw[C - 1][U];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i)
-                if (i < r) load_leaf<DT, V, U, NT>(grads, nfull * C + i, start_bytes, off, raw[i]);
+                if (i < r) load_leaf<DT, V, U>(grads, nfull * C + i, start_bytes, off, raw[i]);
 #pragma unroll
             for (int i = 0; i < C - 1; ++i) {
                 if (i < r) {
@@ -378,7 +370,7 @@ __device__ __forceinline__ void lane_elems(uint32_t count, uint32_t (&idx)[U], b
     }
 }
 
-template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT, int MODE>
+template <int DT, int V, int U, int C, int MAXD, bool TREE, int MODE>
 __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start, uint32_t count,
                                             float lr_j, float wd_j) {
     constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
@@ -392,7 +384,7 @@ __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start,
     }
     const uint64_t start4 = start * 4;
     Acc<U, V> s;
-    reduce<DT, V, U, C, MAXD, TREE, NT>(a.grads, a.K, start * SG, roff, s);
+    reduce<DT, V, U, C, MAXD, TREE>(a.grads, a.K, start * SG, roff, s);
     if constexpr (MODE == MODE_REDUCE) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -421,7 +413,7 @@ __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start,
     }
 }
 
-template <int DT, int V, int U, int C, int MAXD, bool TREE, bool NT, int MODE>
+template <int DT, int V, int U, int C, int MAXD, bool TREE, int MODE>
 __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const Tile tile = ld_tile(a.tiles, t);
@@ -432,9 +424,9 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
             wd_j = a.wd * ldc(a.mults, 2 * j + 1);
         }
         if (!(tile.seg & TAIL_BIT))
-            reduce_body<DT, V, U, C, MAXD, TREE, NT, MODE>(a, tile.start, tile.count, lr_j, wd_j);
+            reduce_body<DT, V, U, C, MAXD, TREE, MODE>(a, tile.start, tile.count, lr_j, wd_j);
         else
-            reduce_body<DT, 1, 1, C, MAXD, TREE, NT, MODE>(a, tile.start, tile.count, lr_j, wd_j);
+            reduce_body<DT, 1, 1, C, MAXD, TREE, MODE>(a, tile.start, tile.count, lr_j, wd_j);
     }
 }
 
@@ -508,49 +500,45 @@ template <int A, int B, class F> hipError_t pick(int x, F&& f) {
     return x == B ? f(I<B>{}) : f(I<A>{});
 }
 
-template <int DT, int TREE, int MODE, int U, int C, int MAXD, int NT>
+// Pending-subtree stack depths compiled (>= bit length of K / kchunk).
+template <class F> hipError_t pick_maxd(int maxd, F&& f) {
+    if (maxd <= 5) return f(I<5>{});
+    if (maxd <= 7) return f(I<7>{});
+    return f(I<MAXD_MAX>{});
+}
+
+// (vectors per lane, replicas per batch) pairs compiled.
+template <class F> hipError_t pick_uc(int u, int c, F&& f) {
+    if (u == 1 && c == 16) return f(I<1>{}, I<16>{});
+    if (u == 1 && c == 8) return f(I<1>{}, I<8>{});
+    if (u == 2 && c == 16) return f(I<2>{}, I<16>{});
+    if (u == 2 && c == 8) return f(I<2>{}, I<8>{});
+    if (u == 4 && c == 8) return f(I<4>{}, I<8>{});
+    if (u == 4 && c == 4) return f(I<4>{}, I<4>{});
+    if (u == 4 && c == 2) return f(I<4>{}, I<2>{});
+    return hipErrorInvalidValue;
+}
+
+template <int DT, int TREE, int MODE, int U, int C, int MAXD>
 hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
     constexpr int V = 4;  // elements per lane-vector for both storage types
-    hipLaunchKernelGGL((reduce_kernel<DT, V, U, C, MAXD, (TREE != 0), (NT != 0), MODE>), dim3(grid),
-                       dim3(block), 0, s, a);
+    hipLaunchKernelGGL((reduce_kernel<DT, V, U, C, MAXD, (TREE != 0), MODE>), dim3(grid), dim3(block), 0, s, a);
     return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_reduce(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
-    return pick<FC_F32, FC_F16>(sh.dtype, [&](auto dt) {
-        return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
-            return pick<1, 2>(sh.vecs, [&](auto u) {
-                return pick<8, 16>(sh.kchunk, [&](auto c) {
-                    return pick<0, 1>(sh.nontemporal, [&](auto nt) {
-                        if (sh.tree) {
-                            return pick<MAXD_SMALL, MAXD_LARGE>(sh.maxd, [&](auto d) {
-                                return go_reduce<dt.value, 1, md.value, u.value, c.value, d.value, nt.value>(
-                                    grid, sh.block, a, s);
-                            });
-                        }
-                        return go_reduce<dt.value, 0, md.value, u.value, c.value, 1, nt.value>(grid, sh.block,
-                                                                                                a, s);
-                    });
+template <int DT>
+hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
+    return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
+        return pick_uc(sh.vecs, sh.kchunk, [&](auto u, auto c) {
+            if (sh.tree) {
+                return pick_maxd(sh.maxd, [&](auto d) {
+                    return go_reduce<DT, 1, md.value, u.value, c.value, d.value>(grid, sh.block, a, s);
                 });
-            });
+            }
+            return go_reduce<DT, 0, md.value, u.value, c.value, 1>(grid, sh.block, a, s);
         });
     });
 }
 
-hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s) {
-    return pick<1, 2>(sh.vecs, [&](auto u) {
-        hipLaunchKernelGGL((sgd_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
-        return hipGetLastError();
-    });
-}
-
-hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s) {
-    return pick<1, 2>(sh.vecs, [&](auto u) {
-        hipLaunchKernelGGL((bcast_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
-        return hipGetLastError();
-    });
-}
-
+}  // namespace
 }  // namespace fc

@@ -29,9 +29,8 @@ struct Shape {
     int dtype;        // fc_dtype
     int tree;         // 1 tree order, 0 linear
     int block;        // threads per block
-    int vecs;         // 4-element lane-vectors per thread (1 or 2)
-    int kchunk;       // replicas loaded per batch (8 or 16)
-    int nontemporal;  // non-temporal replica loads
+    int vecs;         // 4-element lane-vectors per thread (1, 2 or 4)
+    int kchunk;       // replicas loaded per batch (2, 4, 8 or 16; see the pairs compiled)
     int maxd;         // depth of the pending-subtree stack (>= bit length of K / kchunk)
 };
 
@@ -68,12 +67,12 @@ struct BcastArgs {
     int K;
 };
 
-// Largest pending-subtree stack depth compiled; plans whose K / kchunk needs
-// more are rejected at creation.
-constexpr int MAXD_SMALL = 5;
-constexpr int MAXD_LARGE = 9;
+// Largest pending-subtree stack depth compiled (stack depths 5, 7 and 10 are
+// instantiated); plans whose K / kchunk needs more are rejected at creation.
+constexpr int MAXD_MAX = 10;
 
-hipError_t launch_reduce(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
+hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
+hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s);
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s);
 

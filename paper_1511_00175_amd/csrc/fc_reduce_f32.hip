@@ -1,0 +1,10 @@
+// Reduce and fused-step kernels for fp32 replicas.
+#include "fc_device.h"
+
+namespace fc {
+
+hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
+    return launch_reduce_dt<FC_F32>(sh, mode, grid, a, s);
+}
+
+}  // namespace fc

@@ -55,8 +55,8 @@ def test_strerror(fcmod):
     ([(0, 16)], 4, 7, None, -1),                       # bad dtype
     ([(0, 16)], 4, 0, {"block_threads": 96}, -1),      # bad launch shape
     ([(0, 16)], 4, 0, {"vecs_per_thread": 3}, -1),
-    ([(0, 16)], 4, 0, {"kchunk": 4}, -1),
-    ([(0, 16)], 4, 0, {"nontemporal": 2}, -1),
+    ([(0, 16)], 4, 0, {"vecs_per_thread": 1, "kchunk": 4}, -1),   # pair not compiled
+    ([(0, 16)], 4, 0, {"vecs_per_thread": 4, "kchunk": 16}, -1),
     ([(0, 16)], 4, 0, {"max_blocks": -1}, -1),
     ([(0, 16)], 4, 0, {"schedule": 3}, -1),
 ])

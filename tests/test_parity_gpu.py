@@ -99,9 +99,9 @@ def test_fp16_widening_exhaustive(fc):
     assert same_bits(out.cpu().numpy(), ref) == 0
 
 
-SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c, nontemporal=nt)
-          for b in (64, 128, 256) for u in (1, 2) for c in (8, 16) for nt in (0, 1)]
-SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, max_blocks=5)]
+PAIRS = [(1, 8), (1, 16), (2, 8), (2, 16), (4, 2), (4, 4), (4, 8)]
+SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c) for b in (64, 128, 256) for u, c in PAIRS]
+SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, kchunk=8, max_blocks=5)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -111,7 +111,7 @@ def test_launch_shape_invariance(fc, dtype):
     segs = table(5000, dtype)
     K = 37
     ref = None
-    for opts in SHAPES + [dict(max_blocks=7), dict(max_blocks=1, vecs_per_thread=2)]:
+    for opts in SHAPES + [dict(max_blocks=7), dict(max_blocks=1, vecs_per_thread=2, kchunk=16)]:
         bad, got, expect = run_reduce(fc, segs, K, dtype, "tree", np.random.default_rng(5), opts=opts)
         assert bad == 0, opts
         if ref is None:
