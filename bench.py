@@ -138,6 +138,58 @@ def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
             "seconds": round(dt, 3), "us_per_step_equiv": round(dt / n * wl.n_params * 1e6, 1)}
 
 
+def sweep_k(args):
+    """One-GPU analog of Fig. 4 (parameter server vs reduction tree, NiN's 30 MB
+    per worker): for K = 1..128 workers, time fc_tree_reduce in tree and in
+    linear (parameter-server) order over one 7,595,176-parameter (NiN-sized)
+    fp32 vector per worker, and measure each order's rounding error against an
+    fp64 sum.  On one GPU both orders read the same K*N*4 bytes, so time grows
+    linearly in K for both (Eq. 3 vs Eq. 4 is a network cost model); what the
+    order changes is the error bound: gamma_d * sum|x| with d = ceil(log2 K)
+    for the tree, d = K-1 for the linear order.  Prints one JSON line per
+    (K, order)."""
+    import torch
+
+    import paper_1511_00175_amd as fc
+    from workloads import tables
+
+    dev = torch.device("cuda:0")
+    wl = tables.nin()
+    n = wl.n_params
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    kmax = 128
+    stride = (n + 63) // 64 * 64 + 64  # 256-byte aligned replica rows, staggered
+    reps = (torch.randn((kmax, stride), generator=g, device=dev) * 1e-3)
+    out = torch.empty(n, device=dev)
+    rows = [(0, n, 1.0, 1.0)]
+    sample = torch.randint(0, n, (1 << 16,), generator=g, device=dev)
+    u = 2.0 ** -24
+    for K in (1, 2, 4, 8, 16, 32, 64, 128):
+        x = reps[:K]
+        exact = x[:, sample].double().sum(0)
+        absum = x[:, sample].double().abs().sum(0)
+        for order in ("tree", "linear"):
+            plan = fc.Plan(rows, K, "f32", order)
+            plan.set_timing(True)
+            for _ in range(3):
+                plan.tree_reduce(x, out)
+            plan.read_timing()
+            for _ in range(args.sweep_reps):
+                plan.tree_reduce(x, out)
+            torch.cuda.synchronize()
+            launches, total = plan.read_timing()["reduce"]
+            plan.close()
+            rel = ((out[sample].double() - exact).abs() / absum).cpu()
+            d = 0 if K == 1 else (math.ceil(math.log2(K)) if order == "tree" else K - 1)
+            us = total / launches
+            print(json.dumps({"sweep": "fig4_one_gpu", "K": K, "order": order, "n_params": n,
+                              "mb_per_worker": round(4 * n / 1e6, 1), "us": round(us, 2),
+                              "gb_s": round((K * 4 + 4) * n / us / 1e3, 1),
+                              "err_rel_median": float(rel.median()), "err_rel_max": float(rel.max()),
+                              "bound_gamma_d": d * u / (1 - d * u)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -158,6 +210,9 @@ def main():
                     help="after the measurement, run a plain device copy of this many MiB three times "
                          "(reference kernel of known size for hardware byte counters)")
     ap.add_argument("--print-hash", action="store_true", help="print the library source hash and exit")
+    ap.add_argument("--sweep-k", action="store_true",
+                    help="instead of the benchmark line, print the tree vs parameter-server K sweep")
+    ap.add_argument("--sweep-reps", type=int, default=20)
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="do not record per-kernel events (roofline entry then uses the wall time per step)")
     args = ap.parse_args()
@@ -179,6 +234,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(2)
+    if args.sweep_k:
+        sweep_k(args)
+        return
     dev = torch.device("cuda:0")
     wl = tables.get(args.workload)
     opts = {}
