@@ -163,6 +163,44 @@ int fc_broadcast(fc_plan* plan, const float* src, float* const* dst, void* strea
 int fc_step(fc_plan* plan, const void* const* grads, float* w, float* v, float lr, float mu,
             float wd, int batch, float* out, float* const* bcast_dst, void* stream);
 
+/* Learning-rate policies (Sec. 7.2 "Results: Midsized deep models", Sec. 7.3
+ * "Results: Ultra-deep models").  The rate at iteration `iter` for a step of
+ * `batch` samples is, evaluated in double and rounded to float once:
+ *     lr = (base_lr * scale) * factor(iter)
+ *     scale = batch / base_batch     (linear scaling with the batch, Sec. 7.2:
+ *                                     4x the batch -> 4x the rate); 1 when
+ *                                     base_batch == 0
+ *     FIXED: factor = 1
+ *     STEP : factor = gamma ^ floor(iter / stepsize)   (Sec. 7.2: divided by
+ *            10 twice during training -> gamma 0.1)
+ *     POLY : factor = (1 - iter / max_iter) ^ power    (Sec. 7.3, power 0.5),
+ *            0 <= iter <= max_iter
+ * pow() is the C library's. */
+typedef enum { FC_LR_FIXED = 0, FC_LR_STEP = 1, FC_LR_POLY = 2 } fc_lr_kind;
+
+typedef struct {
+    int kind;          /* fc_lr_kind */
+    int base_batch;    /* batch the base rate is quoted for; 0 = no batch scaling */
+    double base_lr;    /* >= 0 */
+    double gamma;      /* STEP: > 0 */
+    int64_t stepsize;  /* STEP: >= 1 */
+    int64_t max_iter;  /* POLY: >= 1 */
+    double power;      /* POLY: >= 0 */
+} fc_lr_policy;
+
+/* *lr = the policy's rate at `iter` (>= 0) for `batch` (>= 1).  Host only;
+ * FC_EINVAL for a bad policy or iteration. */
+int fc_lr_at(const fc_lr_policy* policy, int64_t iter, int batch, float* lr);
+
+/* Multi-step driver: n_iters fused steps (fc_step without raw sum or
+ * broadcast) at iterations first_iter .. first_iter + n_iters - 1, each with
+ * the policy's rate, all enqueued on `stream`.  The same K replicas feed every
+ * step (a driver for benchmarks and tests; in training, call fc_lr_at and
+ * fc_step once per iteration with that iteration's gradients).  Validation as
+ * fc_step; stops at the first error. */
+int fc_train(fc_plan* plan, const void* const* grads, float* w, float* v, const fc_lr_policy* policy,
+             int64_t first_iter, int64_t n_iters, float mu, float wd, int batch, void* stream);
+
 /* Static description of a message code (never NULL). */
 const char* fc_strerror(int code);
 

@@ -39,7 +39,10 @@ class _Lib:
         L.orc_broadcast.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp]
         L.orc_step.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, vp, vp,
                                ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int, vp, vp, vp]
-        for f in ("orc_tree_reduce", "orc_sgd_step", "orc_broadcast", "orc_step"):
+        L.orc_lr_at.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_int64,
+                                ctypes.c_int64, ctypes.c_double, ctypes.c_int64, ctypes.c_int,
+                                ctypes.POINTER(ctypes.c_float)]
+        for f in ("orc_tree_reduce", "orc_sgd_step", "orc_broadcast", "orc_step", "orc_lr_at"):
             getattr(L, f).restype = ctypes.c_int
         self.L = L
         self.path = path
@@ -178,3 +181,25 @@ def step(segs, grads, w, v, lr, mu, wd, batch, order="tree", out=None, bcast=Non
     if rc:
         raise ValueError(f"orc_step failed ({rc})")
     return w, v, out, bcast
+
+
+LR_KINDS = {"fixed": 0, "step": 1, "poly": 2}
+
+
+def lr_at(kind, iter, batch, base_lr, base_batch=0, gamma=0.1, stepsize=1, max_iter=1, power=1.0):
+    """Learning rate of a policy at `iter` (float32)."""
+    out = ctypes.c_float()
+    rc = lib().orc_lr_at(LR_KINDS[kind], base_lr, base_batch, gamma, stepsize, max_iter, power, iter, batch,
+                         ctypes.byref(out))
+    if rc:
+        raise ValueError("invalid learning-rate policy or iteration")
+    return np.float32(out.value)
+
+
+def train(segs, grads, w, v, mu, wd, batch, iters, policy):
+    """Steps at iterations `iters` with the policy's rate (same replicas every
+    step); returns (w, v).  `policy` is a dict of lr_at keyword arguments."""
+    for it in iters:
+        lr = lr_at(iter=it, batch=batch, **policy)
+        w, v, _, _ = step(segs, grads, w, v, float(lr), mu, wd, batch)
+    return w, v

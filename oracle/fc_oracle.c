@@ -43,6 +43,11 @@
  *   - lr_j = lr * lr_mult_j and wd_j = wd * decay_mult_j, each one fp32
  *     rounding; c = 1.0f / (float)batch, one fp32 rounding.
  *
+ * Learning-rate policies (Sec. 7.2: step -- divide by 10 at fixed points --
+ * and the rate scaled with the batch; Sec. 7.3: polynomial decay with power
+ * 0.5): rate = base_lr * (batch / base_batch) * factor(iter), evaluated in
+ * double and rounded to float once.
+ *
  * Pins (see tests): fp16 widening against numpy over all 65536 patterns; K=1
  * identity; all-ones sums to K; integer-valued inputs give the exact integer
  * sum in both orders; the pairwise-summation error bound against an exact
@@ -182,6 +187,31 @@ int orc_broadcast(const orc_segment* segs, int nseg, int K, const float* src, fl
         for (int j = 0; j < nseg; ++j)
             for (uint64_t i = segs[j].offset; i < segs[j].offset + segs[j].length; ++i)
                 dst[k][i] = src[i];
+    return 0;
+}
+
+/* Learning rate at iteration `iter` (kind 0 fixed, 1 step, 2 poly); returns
+ * -1 for an invalid policy or iteration. */
+int orc_lr_at(int kind, double base_lr, int base_batch, double gamma, int64_t stepsize, int64_t max_iter,
+              double power, int64_t iter, int batch, float* lr)
+{
+    if (iter < 0 || batch < 1 || base_batch < 0 || !(base_lr >= 0.0)) return -1;
+    double factor;
+    if (kind == 0) {
+        factor = 1.0;
+    } else if (kind == 1) {
+        if (stepsize < 1 || !(gamma > 0.0)) return -1;
+        int64_t drops = iter / stepsize;              /* completed steps of the schedule */
+        factor = pow(gamma, (double)drops);
+    } else if (kind == 2) {
+        if (max_iter < 1 || iter > max_iter || !(power >= 0.0)) return -1;
+        double remaining = 1.0 - (double)iter / (double)max_iter;
+        factor = pow(remaining, power);
+    } else {
+        return -1;
+    }
+    double scale = (base_batch > 0) ? (double)batch / (double)base_batch : 1.0;
+    *lr = (float)(base_lr * scale * factor);
     return 0;
 }
 

@@ -11,10 +11,20 @@ only marshals torch tensors (device memory and the current stream) into it.
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
                   FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
-                  fc_plan_read_timing, fc_plan_set_timing, fc_sgd_step, fc_step, fc_strerror, fc_tree_reduce)
+                  fc_lr_at, fc_plan_read_timing, fc_plan_set_timing, fc_sgd_step, fc_step, fc_strerror, fc_train,
+                  fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
-           "fc_plan_read_timing", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror"]
+           "fc_plan_read_timing", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
+           "fc_lr_at", "fc_train", "lr_policy", "lr_at"]
+
+
+def lr_at(iter, batch, **policy):
+    """Learning rate of a policy (lr_policy keyword arguments) at `iter`."""
+    rc, lr = fc_lr_at(lr_policy(**policy), iter, batch)
+    if rc:
+        raise FcError("fc_lr_at", rc)
+    return lr
 
 _DTYPES = {"f32": FC_F32, "f16": FC_F16}
 _ORDERS = {"tree": FC_ORDER_TREE, "linear": FC_ORDER_LINEAR}
@@ -99,6 +109,14 @@ class Plan:
         rc = fc_broadcast(self.handle, _ptr(src), _rows(dst), _stream(stream))
         if rc:
             raise FcError("fc_broadcast", rc)
+
+    def train(self, grads, w, v, policy, first_iter, n_iters, mu, wd, batch, stream=None):
+        """n_iters fused steps with the policy's rate (policy: lr_policy
+        keyword arguments); the same replicas feed every step."""
+        rc = fc_train(self.handle, _rows(grads), _ptr(w), _ptr(v), lr_policy(**policy), first_iter, n_iters,
+                      mu, wd, batch, _stream(stream))
+        if rc:
+            raise FcError("fc_train", rc)
 
     def step(self, grads, w, v, lr, mu, wd, batch, out=None, bcast=None, stream=None):
         rc = fc_step(self.handle, _rows(grads), _ptr(w), _ptr(v), lr, mu, wd, batch, _ptr(out),

@@ -43,6 +43,15 @@ class fc_timing(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int * FC_KERNEL_KINDS), ("total_us", ctypes.c_double * FC_KERNEL_KINDS)]
 
 
+FC_LR_FIXED, FC_LR_STEP, FC_LR_POLY = 0, 1, 2
+
+
+class fc_lr_policy(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("base_batch", ctypes.c_int), ("base_lr", ctypes.c_double),
+                ("gamma", ctypes.c_double), ("stepsize", ctypes.c_int64), ("max_iter", ctypes.c_int64),
+                ("power", ctypes.c_double)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
                       "python paper_1511_00175_amd/build.py")
@@ -66,10 +75,13 @@ lib.fc_step.argtypes = [_plan_p, _pp, _vp, _vp, _f, _f, _f, _i, _vp, _pp, _vp]
 lib.fc_strerror.argtypes = [_i]
 lib.fc_strerror.restype = ctypes.c_char_p
 lib.fc_plan_query.argtypes = [_plan_p, ctypes.POINTER(fc_plan_info)]
+lib.fc_lr_at.argtypes = [ctypes.POINTER(fc_lr_policy), ctypes.c_int64, _i, ctypes.POINTER(ctypes.c_float)]
+lib.fc_train.argtypes = [_plan_p, _pp, _vp, _vp, ctypes.POINTER(fc_lr_policy), ctypes.c_int64, ctypes.c_int64,
+                         _f, _f, _i, _vp]
 lib.fc_plan_set_timing.argtypes = [_plan_p, _i]
 lib.fc_plan_read_timing.argtypes = [_plan_p, ctypes.POINTER(fc_timing)]
 for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
-           "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing"):
+           "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing", "fc_lr_at", "fc_train"):
     getattr(lib, _n).restype = ctypes.c_int
 
 
@@ -155,3 +167,25 @@ def fc_broadcast(plan, src, dst, stream=0):
 
 def fc_step(plan, grads, w, v, lr, mu, wd, batch, out=None, bcast_dst=None, stream=0):
     return lib.fc_step(plan, _ptr_array(grads), w, v, lr, mu, wd, int(batch), out, _ptr_array(bcast_dst), stream)
+
+
+_LR_KINDS = {"fixed": FC_LR_FIXED, "step": FC_LR_STEP, "poly": FC_LR_POLY}
+
+
+def lr_policy(kind, base_lr, base_batch=0, gamma=0.1, stepsize=1, max_iter=1, power=1.0):
+    """fc_lr_policy from keyword arguments (kind: "fixed", "step" or "poly")."""
+    return fc_lr_policy(_LR_KINDS[kind], int(base_batch), float(base_lr), float(gamma), int(stepsize),
+                        int(max_iter), float(power))
+
+
+def fc_lr_at(policy, iter, batch):
+    """Returns (rc, lr)."""
+    out = ctypes.c_float()
+    rc = lib.fc_lr_at(ctypes.byref(policy) if policy is not None else None, int(iter), int(batch),
+                      ctypes.byref(out))
+    return rc, out.value
+
+
+def fc_train(plan, grads, w, v, policy, first_iter, n_iters, mu, wd, batch, stream=0):
+    return lib.fc_train(plan, _ptr_array(grads), w, v, ctypes.byref(policy), int(first_iter), int(n_iters),
+                        mu, wd, int(batch), stream)

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -12,6 +13,7 @@
 
 #include "fc.h"
 #include "fc_internal.h"
+#include "fc_shape.h"
 
 using fc::Tile;
 
@@ -121,30 +123,8 @@ void note_stream(fc_plan* p, hipStream_t s) {
     p->have_last_stream = true;
 }
 
-// Launch-shape defaults, measured on MI355X for the five workloads:
-//   fp16 replicas       : 4 vectors per lane, 4 replicas per batch, 256 threads
-//   fp32, 16 < K <= 64  : 4 vectors per lane, 2 replicas per batch, 256 threads
-//   other fp32          : 1 vector per lane, 16 replicas per batch, 64 threads
-// Four vectors per lane make every wave read 4 KiB of one replica at a time,
-// which HBM serves better than 1 KiB pieces, as long as the lane's registers
-// (16 accumulators per pending subtree) still allow enough waves in flight.
-void default_shape(fc_dtype gdt, int K, fc::Shape& sh) {
-    if (gdt == FC_F16) {
-        sh.vecs = 4; sh.kchunk = 4; sh.block = 256;
-    } else if (K > 16 && K <= 64) {
-        sh.vecs = 4; sh.kchunk = 2; sh.block = 256;
-    } else {
-        sh.vecs = 1; sh.kchunk = 16; sh.block = 64;
-    }
-}
-
-bool compiled_pair(int u, int c) {
-    return (u == 1 && (c == 8 || c == 16)) || (u == 2 && (c == 8 || c == 16)) ||
-           (u == 4 && (c == 2 || c == 4 || c == 8));
-}
-
 int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh) {
-    default_shape(gdt, K, sh);
+    fc::default_shape(gdt, K, sh);
     if (!o) return FC_OK;
     if (o->block_threads) {
         if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
@@ -154,7 +134,7 @@ int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh) {
         // an explicit pair replaces the default pair; one field alone keeps the other default
         const int u = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
         const int c = o->kchunk ? o->kchunk : sh.kchunk;
-        if (!compiled_pair(u, c)) return FC_EINVAL;
+        if (!fc::compiled_pair(u, c)) return FC_EINVAL;
         sh.vecs = u;
         sh.kchunk = c;
     }
@@ -335,10 +315,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
 
     // fc_step schedule: two passes when the replicas dominate the bytes (see fc_schedule)
     const int sched = opts ? opts->schedule : FC_SCHED_AUTO;
-    if (sched == FC_SCHED_AUTO)
-        p->schedule = (static_cast<int64_t>(K) * p->sg > 256) ? FC_SCHED_TWO_PASS : FC_SCHED_FUSED;
-    else
-        p->schedule = sched;
+    p->schedule = sched == FC_SCHED_AUTO ? fc::default_schedule(K, p->sg) : sched;
 
     if (hipGetDevice(&p->device) != hipSuccess) {
         delete p;
@@ -589,6 +566,47 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     rc = launch(p, FC_KERNEL_STEP, s, [&] { return launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
     note_stream(p, s);
     return rc;
+}
+
+int fc_lr_at(const fc_lr_policy* pol, int64_t iter, int batch, float* lr) {
+    if (!pol || !lr || iter < 0 || batch < 1) return FC_EINVAL;
+    if (!(pol->base_lr >= 0.0) || pol->base_batch < 0) return FC_EINVAL;
+    double factor = 1.0;
+    switch (pol->kind) {
+        case FC_LR_FIXED:
+            break;
+        case FC_LR_STEP:
+            if (pol->stepsize < 1 || !(pol->gamma > 0.0)) return FC_EINVAL;
+            factor = std::pow(pol->gamma, static_cast<double>(iter / pol->stepsize));
+            break;
+        case FC_LR_POLY:
+            if (pol->max_iter < 1 || iter > pol->max_iter || !(pol->power >= 0.0)) return FC_EINVAL;
+            factor = std::pow(1.0 - static_cast<double>(iter) / static_cast<double>(pol->max_iter), pol->power);
+            break;
+        default:
+            return FC_EINVAL;
+    }
+    const double scale =
+        pol->base_batch > 0 ? static_cast<double>(batch) / static_cast<double>(pol->base_batch) : 1.0;
+    *lr = static_cast<float>(pol->base_lr * scale * factor);
+    return FC_OK;
+}
+
+int fc_train(fc_plan* p, const void* const* grads, float* w, float* v, const fc_lr_policy* policy,
+             int64_t first_iter, int64_t n_iters, float mu, float wd, int batch, void* stream) {
+    if (!p || !policy || first_iter < 0 || n_iters < 0) return FC_EINVAL;
+    float lr = 0.0f;
+    // check the whole schedule before enqueuing anything
+    if (n_iters > 0) {
+        int rc = fc_lr_at(policy, first_iter + n_iters - 1, batch, &lr);
+        if (rc) return rc;
+    }
+    for (int64_t it = first_iter; it < first_iter + n_iters; ++it) {
+        int rc = fc_lr_at(policy, it, batch, &lr);
+        if (rc == FC_OK) rc = fc_step(p, grads, w, v, lr, mu, wd, batch, nullptr, nullptr, stream);
+        if (rc) return rc;
+    }
+    return FC_OK;
 }
 
 }  // extern "C"

@@ -305,7 +305,41 @@ def pin_step_composition():
         assert _same(d[:33], w1[:33]) and _same(d[64:104], w1[64:104])
 
 
+# ------------------------------------------------------------------ learning-rate policies
+def pin_lr_paper_values():
+    """Sec. 7.2: NiN at batch 256 starts at 0.01 and is divided by 10 twice;
+    at batch 1024 the rate is scaled by the same factor as the batch (0.04,
+    Table 2).  Sec. 7.3: GoogLeNet at batch 1024 starts at 0.08."""
+    step = dict(kind="step", base_lr=0.01, gamma=0.1, stepsize=1000)
+    assert oracle.lr_at(iter=0, batch=256, **step) == np.float32(0.01)
+    assert oracle.lr_at(iter=999, batch=256, **step) == np.float32(0.01)
+    assert oracle.lr_at(iter=1000, batch=256, **step) == np.float32(0.001)
+    assert oracle.lr_at(iter=2000, batch=256, **step) == np.float32(0.0001)
+    assert oracle.lr_at("fixed", 0, 1024, 0.01, base_batch=256) == np.float32(0.04)
+    assert oracle.lr_at("fixed", 0, 256, 0.01, base_batch=256) == np.float32(0.01)
+    assert oracle.lr_at("poly", 0, 1024, 0.08, max_iter=10, power=0.5) == np.float32(0.08)
+
+
+def pin_lr_poly_closed_forms():
+    """Sec. 7.3 poly policy base * (1 - iter/max_iter)^power: the end of the
+    run is 0; power 1 is a straight line; power 0.5 and 2 at points where the
+    root and square are exact."""
+    assert oracle.lr_at("poly", 8, 32, 0.5, max_iter=8, power=0.5) == 0.0
+    assert oracle.lr_at("poly", 3, 32, 0.5, max_iter=8, power=1.0) == np.float32(0.3125)
+    assert oracle.lr_at("poly", 3, 32, 0.08, max_iter=4, power=0.5) == np.float32(0.04)
+    assert oracle.lr_at("poly", 1, 32, 0.08, max_iter=2, power=2.0) == np.float32(0.02)
+    for bad in (dict(kind="poly", iter=9, max_iter=8), dict(kind="step", iter=1, stepsize=0),
+                dict(kind="fixed", iter=-1)):
+        kw = dict(batch=32, base_lr=0.1)
+        kw.update(bad)
+        try:
+            oracle.lr_at(**kw)
+        except ValueError:
+            continue
+        raise AssertionError(f"invalid policy accepted: {bad}")
+
+
 PINS = [pin_f16_widen_exhaustive, pin_k1_identity, pin_all_ones, pin_integer_exact, pin_fsum_bound,
         pin_order_golden, pin_tree_structure, pin_linear_structure, pin_ieee_special_sums,
         pin_ragged_segments_and_padding, pin_sgd_golden, pin_sgd_fp64_bound, pin_sgd_closed_forms,
-        pin_broadcast, pin_step_composition]
+        pin_broadcast, pin_step_composition, pin_lr_paper_values, pin_lr_poly_closed_forms]

@@ -56,6 +56,9 @@ MUTANTS = {
                                "if (bcast_dst) orc_broadcast(segs, nseg, K, w, bcast_dst);\n"
                                "    rc = orc_sgd_step(segs, nseg, w, v, scratch, lr, mu, wd, batch);\n"
                                "    if (rc) return rc;\n    bcast_dst = 0;")],
+    "lr_poly_power_dropped": [("factor = pow(remaining, power);", "factor = remaining;")],
+    "lr_step_off_by_one": [("int64_t drops = iter / stepsize;", "int64_t drops = (iter + 1) / stepsize;")],
+    "lr_scale_inverted": [("(double)batch / (double)base_batch", "(double)base_batch / (double)batch")],
 }
 
 
