@@ -93,9 +93,11 @@ typedef enum { FC_SCHED_AUTO = 0, FC_SCHED_FUSED = 1, FC_SCHED_TWO_PASS = 2 } fc
 
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero selects the default, which depends on the
- * replica type and K (measured on MI355X): fp16 -> (4 vectors, 4 replicas,
- * 256 threads); fp32 with 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16,
- * 64).  Replica loads always carry the streaming (nt) hint. */
+ * replica type, K and the plan's size (measured on MI355X): fp32 in tree order
+ * with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8 waves (see
+ * k_waves); otherwise fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
+ * 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads
+ * always carry the streaming (nt) hint. */
 typedef struct {
     int block_threads;   /* 64, 128 or 256 threads per block */
     int vecs_per_thread; /* 4-element lane-vectors per thread (1, 2 or 4) ... */
@@ -103,6 +105,19 @@ typedef struct {
                             (1, 8) (1, 16) (2, 8) (2, 16) (4, 2) (4, 4) (4, 8) */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
     int schedule;        /* fc_schedule of fc_step (default FC_SCHED_AUTO) */
+    int k_waves;         /* tree order only: 4, 8 or 16 waves of a block split the K
+                            replicas between them (block_threads 64 * k_waves;
+                            wave q reduces an aligned run of replicas, a complete
+                            subtree of the tree, and the block combines the runs
+                            in tree order through LDS).
+                            Compiled (k_waves, vecs_per_thread, kchunk): (4, 4, 2)
+                            (8, 4, 2) (16, 4, 2) (8, 2, 4) (16, 2, 4) (16, 2, 2); a
+                            wave's run may span at most 8 batches of kchunk
+                            (K <= 8 * kchunk * k_waves), else FC_EINVAL.  With a
+                            split, vecs_per_thread and kchunk default to 4 and 2.
+                            1: no split.
+                            0: the default, or no split when another shape field
+                            is given. */
 } fc_launch_opts;
 
 /* Create a plan for K workers over a segment table (Sec. 6: one gradient
@@ -219,6 +234,7 @@ typedef struct {
     int kchunk;
     int schedule;        /* resolved fc_schedule of fc_step: FUSED or TWO_PASS */
     uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
+    int k_waves;         /* waves splitting the K replicas (1: no split) */
 } fc_plan_info;
 
 int fc_plan_query(const fc_plan* plan, fc_plan_info* info);

@@ -59,7 +59,7 @@ class Plan:
     dtype   : replica storage, "f32" or "f16".
     order   : "tree" (reduction tree) or "linear" (parameter server).
     opts    : launch shape (block_threads, vecs_per_thread, kchunk,
-              max_blocks) and fc_step schedule (0 auto, 1 fused,
+              max_blocks, k_waves) and fc_step schedule (0 auto, 1 fused,
               2 two-pass); results do not depend on them.
     """
 

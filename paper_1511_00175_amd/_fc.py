@@ -23,7 +23,7 @@ class fc_segment(ctypes.Structure):
 
 class fc_launch_opts(ctypes.Structure):
     _fields_ = [("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int), ("kchunk", ctypes.c_int),
-                ("max_blocks", ctypes.c_int), ("schedule", ctypes.c_int)]
+                ("max_blocks", ctypes.c_int), ("schedule", ctypes.c_int), ("k_waves", ctypes.c_int)]
 
 
 class fc_plan_info(ctypes.Structure):
@@ -31,7 +31,7 @@ class fc_plan_info(ctypes.Structure):
                 ("n_elems", ctypes.c_uint64), ("extent", ctypes.c_uint64), ("ntiles", ctypes.c_int),
                 ("grid", ctypes.c_int), ("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int),
                 ("kchunk", ctypes.c_int), ("schedule", ctypes.c_int),
-                ("scratch_bytes", ctypes.c_uint64)]
+                ("scratch_bytes", ctypes.c_uint64), ("k_waves", ctypes.c_int)]
 
 
 FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS = 0, 1, 2
@@ -125,7 +125,7 @@ def fc_plan_create(segs, K, gdt=FC_F32, order=FC_ORDER_TREE, opts=None):
     if opts is None:
         rc = lib.fc_plan_create(ctypes.byref(h), arr, n, int(K), int(gdt), int(order))
     else:
-        o = fc_launch_opts(0, 0, 0, 0, 0)
+        o = fc_launch_opts(0, 0, 0, 0, 0, 0)
         for k, v in opts.items():
             setattr(o, k, int(v))
         rc = lib.fc_plan_create_ex(ctypes.byref(h), arr, n, int(K), int(gdt), int(order), ctypes.byref(o))

@@ -123,23 +123,51 @@ void note_stream(fc_plan* p, hipStream_t s) {
     p->have_last_stream = true;
 }
 
-int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh) {
+int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc_order order, int K, uint64_t n_elems,
+                  fc::Shape& sh) {
     fc::default_shape(gdt, K, sh);
-    if (!o) return FC_OK;
-    if (o->block_threads) {
-        if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
-        sh.block = o->block_threads;
+    int w = fc::default_kwaves(gdt, order, K, n_elems);
+    int u = 4, c = 2;  // lane vectors and batch of a K split
+    if (o) {
+        if (o->k_waves < 0 || o->max_blocks < 0) return FC_EINVAL;
+        if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_TWO_PASS) return FC_EINVAL;
+        // an explicit shape without k_waves asks for the unsplit kernel
+        const bool shape_given = o->block_threads || o->vecs_per_thread || o->kchunk;
+        if (o->k_waves) w = o->k_waves;
+        else if (shape_given) w = 1;
+        if (w > 1) {
+            if (o->vecs_per_thread) u = o->vecs_per_thread;
+            if (o->kchunk) c = o->kchunk;
+            if (o->block_threads && o->block_threads != 64 * w) return FC_EINVAL;
+        } else {
+            if (o->block_threads) {
+                if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
+                sh.block = o->block_threads;
+            }
+            if (o->vecs_per_thread || o->kchunk) {
+                // an explicit pair replaces the default pair; one field alone keeps the other default
+                const int pu = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
+                const int pc = o->kchunk ? o->kchunk : sh.kchunk;
+                if (!fc::compiled_pair(pu, pc)) return FC_EINVAL;
+                sh.vecs = pu;
+                sh.kchunk = pc;
+            }
+        }
     }
-    if (o->vecs_per_thread || o->kchunk) {
-        // an explicit pair replaces the default pair; one field alone keeps the other default
-        const int u = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
-        const int c = o->kchunk ? o->kchunk : sh.kchunk;
-        if (!fc::compiled_pair(u, c)) return FC_EINVAL;
+    if (w > 1) {
+        if (order != FC_ORDER_TREE || !fc::compiled_ksplit(w, u, c)) return FC_EINVAL;
+        sh.kwaves = w;
         sh.vecs = u;
         sh.kchunk = c;
+        sh.block = 64 * w;
+        sh.span = fc::ksplit_span(K, w, c);
+        if (sh.span / c > fc::KSPLIT_MAX_BATCHES) return FC_EINVAL;
+        sh.lanes = 64;
+    } else {
+        sh.kwaves = 1;
+        sh.span = K;
+        sh.lanes = sh.block;
     }
-    if (o->max_blocks < 0) return FC_EINVAL;
-    if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_TWO_PASS) return FC_EINVAL;
     return FC_OK;
 }
 
@@ -233,10 +261,6 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     if (K < 1 || K > K_MAX) return FC_EINVAL;
     if (gdt != FC_F32 && gdt != FC_F16) return FC_EINVAL;
     if (order != FC_ORDER_TREE && order != FC_ORDER_LINEAR) return FC_EINVAL;
-    fc::Shape sh{};
-    int rc = validate_opts(opts, gdt, K, sh);
-    if (rc) return rc;
-
     const int vec = 4;
     uint64_t end = 0, n_elems = 0;
     for (int j = 0; j < nseg; ++j) {
@@ -249,6 +273,9 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     }
     // byte offsets of every element must fit in 64 bits for every buffer
     if (end > (UINT64_MAX / 8)) return FC_EINVAL;
+    fc::Shape sh{};
+    int rc = validate_opts(opts, gdt, order, K, n_elems, sh);
+    if (rc) return rc;
 
     fc_plan* p = new (std::nothrow) fc_plan();
     if (!p) return FC_ENOMEM;
@@ -262,21 +289,21 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     sh.dtype = gdt;
     sh.tree = order == FC_ORDER_TREE;
     const int need = bit_length(K / sh.kchunk);
-    if (need > fc::MAXD_MAX) {
+    if (sh.kwaves == 1 && need > fc::MAXD_MAX) {
         delete p;
         return FC_EINVAL;
     }
-    sh.maxd = need;
+    sh.maxd = sh.kwaves == 1 ? need : fc::KSPLIT_MAXD;
     p->shape = sh;
 
-    // Tile map: each segment is cut into tiles of at most block*vecs vectors;
+    // Tile map: each segment is cut into tiles of at most lanes*vecs vectors;
     // a length that is not a multiple of the vector width leaves a tail tile.
     std::vector<Tile> tiles;
     std::vector<float> mults;
     try {
         p->segs.assign(segs, segs + nseg);
         mults.resize(2 * static_cast<size_t>(std::max(nseg, 1)));
-        const uint64_t tile_vecs = static_cast<uint64_t>(sh.block) * sh.vecs;
+        const uint64_t tile_vecs = static_cast<uint64_t>(sh.lanes) * sh.vecs;
         for (int j = 0; j < nseg; ++j) {
             const fc_segment& s = segs[j];
             mults[2 * j] = s.lr_mult;
@@ -361,6 +388,7 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->kchunk = p->shape.kchunk;
     info->schedule = p->schedule;
     info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
+    info->k_waves = p->shape.kwaves;
     return FC_OK;
 }
 
@@ -439,6 +467,7 @@ int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* strea
     a.mults = p->d_mults;
     a.grads = p->d_grads;
     a.K = p->K;
+    a.span = p->shape.span;
     a.out = out;
     rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s); });
     note_stream(p, s);
@@ -528,6 +557,7 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
         r.mults = p->d_mults;
         r.grads = p->d_grads;
         r.K = p->K;
+        r.span = p->shape.span;
         r.out = sum;
         rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, r, s); });
         if (rc == FC_OK) {
@@ -555,6 +585,7 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     a.mults = p->d_mults;
     a.grads = p->d_grads;
     a.K = p->K;
+    a.span = p->shape.span;
     a.w = w;
     a.v = v;
     a.out = out;

@@ -430,6 +430,120 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ K split across waves
+// A block of W waves shares one tile of 64*U lane-vectors.  The K leaves are
+// cut into aligned runs of S = a.span leaves (a power of two, a multiple of
+// C): wave q < nq = K / S reduces run q, which is a complete subtree of the
+// reduction tree; when K is not a multiple of S, wave nq reduces the r = K -
+// nq*S leaves left over, folding its pending subtrees newest first exactly as
+// reduce() does.  Those subtrees are all smaller than S, so over the whole
+// counter they never merge with a run: the binary counter over K leaves is the
+// counter over the nq run sums, folded onto the left-over value as the newest
+// term.  The partial sums meet in LDS, where one thread per lane-vector
+// finishes the tree that way.  Each wave streams 64*U contiguous vectors of
+// each of its replicas (4 KiB of fp32 for U = 4) while holding a stack for
+// only S leaves.
+template <int DT, int W, int V, int U, int C, int MODE>
+__device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, uint64_t start, uint32_t count,
+                                            float lr_j, float wd_j) {
+    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
+    constexpr int WAVE = 64;
+    constexpr int DC = ilog2<W>() + 1;  // counter over at most W runs
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+    const int S = a.span;
+    const int nq = a.K / S;
+    const int r = a.K - nq * S;
+    if (q < nq || (q == nq && r)) {
+        uint32_t roff[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t vi = lane + u * WAVE;
+            roff[u] = (vi < count ? vi : 0u) * V * SG;  // idle lanes re-read vector 0
+        }
+        Acc<U, V> x;
+        reduce<DT, V, U, C, KSPLIT_MAXD, true>(a.grads + q * S, q < nq ? S : r, start * SG, roff, x);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < V; ++i) part[((q * U + u) * WAVE + lane) * V + i] = x.a[u][i];
+    }
+    __syncthreads();
+    const uint64_t start4 = start * 4;
+    for (int e = threadIdx.x; e < U * WAVE; e += W * WAVE) {
+        // tile vector e = lane e % 64, vector e / 64: its partials sit at (q*U*64 + e)*V
+        Acc<1, V> acc;
+        if (nq == W && !r) {
+            // K = W * S: the W runs are the leaves of one balanced subtree; the
+            // combine's latency is exposed to the whole block, so keep it short
+            Acc<1, V> y[W];
+#pragma unroll
+            for (int n = 0; n < W; ++n)
+#pragma unroll
+                for (int i = 0; i < V; ++i) y[n].a[0][i] = part[(n * U * WAVE + e) * V + i];
+#pragma unroll
+            for (int h = W / 2; h >= 1; h /= 2) {
+#pragma unroll
+                for (int m = 0; m < h; ++m) {
+                    add_right(y[2 * m], y[2 * m + 1]);
+                    if (m) set(y[m], y[2 * m]);
+                }
+            }
+            set(acc, y[0]);
+        } else {
+            Acc<1, V> st[DC];
+            bool have = false;
+            if (r) {
+#pragma unroll
+                for (int i = 0; i < V; ++i) acc.a[0][i] = part[(nq * U * WAVE + e) * V + i];
+                have = true;
+            }
+            for (int n = 0; n < nq; ++n) {
+                Acc<1, V> p;
+#pragma unroll
+                for (int i = 0; i < V; ++i) p.a[0][i] = part[(n * U * WAVE + e) * V + i];
+                push<DC>(st, p, n);
+            }
+            fold<DC>(st, nq, acc, have);
+        }
+        if (static_cast<uint32_t>(e) >= count) continue;
+        const uint32_t off = static_cast<uint32_t>(e) * V * 4;
+        if constexpr (MODE == MODE_REDUCE) {
+            st32r<V>(gwrite(a.out) + start4, off, acc.a[0]);
+        } else {
+            float w[V], v[V], wn[V], vn[V];
+            ld32s<V>(gread(a.w) + start4, off, w);
+            ld32s<V>(gread(a.v) + start4, off, v);
+#pragma unroll
+            for (int i = 0; i < V; ++i) sgd1(acc.a[0][i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
+            st32r<V>(gwrite(a.w) + start4, off, wn);
+            st32r<V>(gwrite(a.v) + start4, off, vn);
+            if (a.out) st32r<V>(gwrite(a.out) + start4, off, acc.a[0]);
+            if (a.dst)
+                for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
+        }
+    }
+    __syncthreads();  // the partials are overwritten by the block's next tile
+}
+
+template <int DT, int W, int U, int C, int MODE>
+__global__ __launch_bounds__(64 * W) void ksplit_kernel(ReduceArgs a) {
+    __shared__ float part[W * U * 64 * 4];
+    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+        const Tile tile = ld_tile(a.tiles, t);
+        float lr_j = 0.0f, wd_j = 0.0f;
+        if constexpr (MODE == MODE_STEP) {
+            const int j = static_cast<int>(tile.seg & SEG_MASK);
+            lr_j = a.lr * ldc(a.mults, 2 * j);
+            wd_j = a.wd * ldc(a.mults, 2 * j + 1);
+        }
+        if (!(tile.seg & TAIL_BIT))
+            ksplit_body<DT, W, 4, U, C, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
+        else
+            ksplit_body<DT, W, 1, 1, C, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
+    }
+}
+
 // ------------------------------------------------------------------ SGD from a raw sum
 template <int V, int U>
 __device__ __forceinline__ void sgd_body(const SgdArgs& a, uint64_t start, uint32_t count, float lr_j,
@@ -526,8 +640,32 @@ hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// (waves, lane vectors, replicas per batch) triples compiled for the K split.
+template <class F> hipError_t pick_ksplit(int w, int u, int c, F&& f) {
+    if (u == 4 && c == 2) {
+        if (w == 4) return f(I<4>{}, I<4>{}, I<2>{});
+        if (w == 8) return f(I<8>{}, I<4>{}, I<2>{});
+        if (w == 16) return f(I<16>{}, I<4>{}, I<2>{});
+    }
+    if (u == 2 && c == 4) {
+        if (w == 8) return f(I<8>{}, I<2>{}, I<4>{});
+        if (w == 16) return f(I<16>{}, I<2>{}, I<4>{});
+    }
+    if (u == 2 && c == 2 && w == 16) return f(I<16>{}, I<2>{}, I<2>{});
+    return hipErrorInvalidValue;
+}
+
 template <int DT>
 hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
+    if (sh.kwaves > 1) {
+        return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
+            return pick_ksplit(sh.kwaves, sh.vecs, sh.kchunk, [&](auto w, auto u, auto c) {
+                hipLaunchKernelGGL((ksplit_kernel<DT, w.value, u.value, c.value, md.value>), dim3(grid),
+                                   dim3(64 * w.value), 0, s, a);
+                return hipGetLastError();
+            });
+        });
+    }
     return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
         return pick_uc(sh.vecs, sh.kchunk, [&](auto u, auto c) {
             if (sh.tree) {

@@ -65,6 +65,24 @@ def test_plan_argument_errors(fcmod, segs, K, gdt, opts, code):
     assert rc == code and not h.value
 
 
+@pytest.mark.parametrize("K,order,opts", [
+    (8, 1, {"k_waves": 4}),                             # split needs the tree order
+    (65, 0, {"k_waves": 4}),                            # a run would take more than 8 batches
+    (257, 0, {"k_waves": 16}),
+    (257, 0, {"k_waves": 8, "vecs_per_thread": 2, "kchunk": 4}),
+    (8, 0, {"k_waves": 8, "vecs_per_thread": 2, "kchunk": 2}),  # triple not compiled
+    (8, 0, {"k_waves": 2}),                             # waves not compiled
+    (8, 0, {"k_waves": 32}),
+    (8, 0, {"k_waves": -1}),
+    (8, 0, {"k_waves": 4, "block_threads": 256 + 64}),  # block must be 64 * waves
+    (8, 0, {"k_waves": 4, "kchunk": 4}),                # triple not compiled
+    (8, 0, {"k_waves": 4, "vecs_per_thread": 1}),
+])
+def test_ksplit_option_errors(fcmod, K, order, opts):
+    rc, h = fcmod._fc.fc_plan_create([(0, 16)], K, 0, order, opts)
+    assert rc == fcmod._fc.FC_EINVAL and not h.value
+
+
 def test_null_arguments(fcmod):
     f = fcmod._fc
     assert f.lib.fc_plan_create(None, None, 0, 1, 0, 0) == f.FC_EINVAL
