@@ -133,20 +133,54 @@ def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
         dt = time.perf_counter() - t0
         return dt, sum(n for _, n, _, _ in rows)
 
+    def run_threads(m, nthreads, repeats=3):
+        # the same window cut into element ranges, one oracle call per range
+        # on its own host thread (ctypes releases the GIL); every element's
+        # arithmetic and order are unchanged
+        from concurrent.futures import ThreadPoolExecutor
+        rows = window(m)
+        r = reps[:, :m].cpu().numpy()
+        wh = w[:m].cpu().numpy()
+        vh = v[:m].cpu().numpy()
+        cuts = [m * i // nthreads for i in range(nthreads + 1)]
+        jobs = []
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            sub = [(max(o, a) - a, min(o + n, b) - max(o, a), lm, dm) for (o, n, lm, dm) in rows
+                   if max(o, a) < min(o + n, b)]
+            if sub:
+                jobs.append((sub, [r[k, a:b] for k in range(r.shape[0])], wh[a:b], vh[a:b]))
+
+        def one(job):
+            sub, rr, ww, vv = job
+            oracle.step(sub, rr, ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, order=order)
+
+        best = float("inf")
+        with ThreadPoolExecutor(nthreads) as ex:
+            for _ in range(repeats):
+                t0 = time.perf_counter()
+                list(ex.map(one, jobs))
+                best = min(best, time.perf_counter() - t0)
+        return best
+
     total = int(ends.max())
     m = min(total, 1 << 16)
     dt, n = run(m)
-    # grow the window to about target_s seconds of oracle work
+    # grow the window to about target_s seconds of single-thread oracle work
     m2 = min(total, int(m * target_s / max(dt, 1e-6)))
     if m2 > m:
         dt, n = run(m2)
         m = m2
     bytes_ = n * (wl.K * wl.s_g + 16)
     model, ncpu = host_info()
-    return {"value": round(bytes_ / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    # the machine's CPU share: OMP_NUM_THREADS when set, else every core
+    nthreads = max(1, min(ncpu or 1, int(os.environ.get("OMP_NUM_THREADS", ncpu or 1))))
+    dt_mt = run_threads(m, nthreads)
+    return {"value": round(bytes_ / dt_mt / 1e9, 4), "unit": "GB/s", "cores": nthreads, "kind": "oracle",
             "sample": f"{n} of {wl.n_params} parameters (elements [0, {m}) of the layout), all K={wl.K} "
-                      f"replicas, one fused step; {dt:.2f} s on 1 thread of {ncpu} ({model})",
-            "seconds": round(dt, 3), "us_per_step_equiv": round(dt / n * wl.n_params * 1e6, 1)}
+                      f"replicas, one fused step, cut into {nthreads} element ranges run on {nthreads} host "
+                      f"threads (best of 3: {dt_mt:.3f} s) of {ncpu} ({model})",
+            "seconds": round(dt_mt, 3), "us_per_step_equiv": round(dt_mt / n * wl.n_params * 1e6, 1),
+            "single_thread": {"value": round(bytes_ / dt / 1e9, 4), "seconds": round(dt, 3), "cores": 1}}
 
 
 def sweep_k(args):
@@ -201,6 +235,72 @@ def sweep_k(args):
                               "bound_gamma_d": d * u / (1 - d * u)}), flush=True)
 
 
+def graph_steps(plan, wl, inputs, out, bcast, n):
+    """Capture n consecutive steps on one input set in one HIP graph (the
+    plan's device tables already hold these pointers, so the captured calls
+    are kernel launches only) and time its replays; returns µs per step."""
+    import torch
+
+    r, w, v = inputs
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            plan.step(r, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(n):
+            plan.step(r, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            g.replay()
+        s.synchronize()
+        reps = max(1, 2000 // n)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            g.replay()
+        e1.record(s)
+    s.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * n)
+    return {"us_per_step": round(us, 3), "steps_per_graph": n, "replays": reps,
+            "value": round(wl.algorithmic_bytes() / us / 1e3, 2), "input_sets": 1}
+
+
+def bandwidth_probes(dev):
+    """Bandwidth ceilings measured on this GPU: the library's streaming read
+    probe over 4 GiB, and torch's device copy of 1 GiB (1 GiB read + 1 GiB
+    written); best of 10, GB/s."""
+    import torch
+
+    import paper_1511_00175_amd as fc
+
+    def best(fn, nbytes, n=10):
+        fn()
+        torch.cuda.synchronize()
+        t = float("inf")
+        for _ in range(n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t = min(t, e0.elapsed_time(e1) * 1e-3)
+        return nbytes / t / 1e9
+
+    x = torch.ones(1 << 30, device=dev)
+    part = torch.empty(fc.fc_read_probe_blocks(4 << 30), device=dev)
+    read = best(lambda: fc.read_probe(x, part), 4 << 30)
+    del x, part
+    a = torch.ones(1 << 28, device=dev)
+    b = torch.empty_like(a)
+    copy = best(lambda: b.copy_(a), 2 << 30)
+    del a, b
+    return {"read_gbs": round(read, 1), "copy_gbs": round(copy, 1),
+            "read": "fc_read_probe over 4 GiB", "copy": "torch copy of 1 GiB (bytes read + written)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,6 +326,11 @@ def main():
     ap.add_argument("--sweep-reps", type=int, default=20)
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="do not record per-kernel events (roofline entry then uses the wall time per step)")
+    ap.add_argument("--graph", type=int, default=0,
+                    help="also capture this many steps (one input set) in one HIP graph and report the "
+                         "graph-amortized time per step")
+    ap.add_argument("--no-probes", action="store_true",
+                    help="skip the read and copy bandwidth probes reported beside the roofline")
     ap.add_argument("--rotate", type=int, default=DEFAULT_ROTATE,
                     help="R independent input sets (replicas, w, v), step i using set i mod R, so that no "
                          "step finds the previous step's w and v in a cache (1: one set)")
@@ -266,15 +371,19 @@ def main():
     reps, w, v = sets[0]
     out = torch.zeros_like(w) if args.out else None
     bcast = torch.zeros((wl.K, wl.padded), device=dev) if args.bcast else None
-    plan = fc.Plan(wl.table(), wl.K, wl.dtype, args.order, **opts)
+    # one plan per input set: each plan's device pointer table then stays
+    # valid from step to step, as in a training loop that reuses its buffers
+    plans = [fc.Plan(wl.table(), wl.K, wl.dtype, args.order, **opts) for _ in sets]
+    plan = plans[0]
     info = plan.info()
     torch.cuda.synchronize()
     count = [0]
 
     def step():
-        r, ww, vv = sets[count[0] % len(sets)]
+        i = count[0] % len(sets)
         count[0] += 1
-        plan.step(r, ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
+        r, ww, vv = sets[i]
+        plans[i].step(r, ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
 
     for _ in range(args.warmup):
         step()
@@ -290,16 +399,24 @@ def main():
     # events add small gaps between kernels, so `value` comes from region 1
     timing = {}
     if not args.no_kernel_timing:
-        plan.set_timing(True)
-        plan.read_timing()
+        for p in plans:
+            p.set_timing(True)
+            p.read_timing()
         for i in range(args.steps):
             step()
         torch.cuda.synchronize()
-        timing = plan.read_timing()
-        plan.set_timing(False)
+        for p in plans:
+            for k, (n, us) in p.read_timing().items():
+                n0, us0 = timing.get(k, (0, 0.0))
+                timing[k] = (n0 + n, us0 + us)
+            p.set_timing(False)
+    graph = None
+    if args.graph > 0:
+        graph = graph_steps(plan, wl, sets[0], out, bcast, args.graph)
     for _ in range(args.profile_loop):
         step()
     torch.cuda.synchronize()
+    probes = None if args.no_probes else bandwidth_probes(dev)
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, device=dev)
@@ -368,9 +485,15 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if probes:
+        res["config"]["probes"] = probes
+        res["roofline"]["frac_of_read_probe"] = round(achieved / probes["read_gbs"], 4)
+    if graph:
+        res["graph"] = graph
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, reps, w, v, args.order, args.cpu_seconds)
-    plan.close()
+    for p in plans:
+        p.close()
     print(json.dumps(res), flush=True)
 
 

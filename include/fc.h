@@ -40,6 +40,11 @@
  *     that call was on another stream (the library then waits for that
  *     stream before replacing the table).  Calls on one plan must not run
  *     concurrently from several host threads.
+ *   - Graph capture: a call whose replica and destination pointers equal
+ *     the plan's previous call, on the same stream, with timing off,
+ *     enqueues kernel launches only (no copies, no memsets, no waits), so it
+ *     may be captured in a HIP graph; run it once eagerly on the capture
+ *     stream first.
  *   - Return value: FC_OK (0) or a negative error code (fc_strerror names
  *     it).  Argument errors are detected before anything is enqueued.
  */
@@ -215,6 +220,16 @@ int fc_lr_at(const fc_lr_policy* policy, int64_t iter, int batch, float* lr);
  * fc_step; stops at the first error. */
 int fc_train(fc_plan* plan, const void* const* grads, float* w, float* v, const fc_lr_policy* policy,
              int64_t first_iter, int64_t n_iters, float mu, float wd, int batch, void* stream);
+
+/* Read-bandwidth probe, for benchmarks: one streaming read of `bytes`
+ * (a multiple of 16, > 0) from the device buffer `src` (16-byte aligned), the
+ * access pattern that bounds any read-bound kernel on this GPU.  Every block
+ * of 16 KiB stores one fp32 partial sum of its bytes read as fp32 into
+ * out[block] (the rounding order is not specified; the sums only keep the
+ * loads live), so `out` must hold fc_read_probe_blocks(bytes) floats.
+ * Asynchronous on `stream`. */
+uint64_t fc_read_probe_blocks(uint64_t bytes);
+int fc_read_probe(const void* src, uint64_t bytes, float* out, void* stream);
 
 /* Static description of a message code (never NULL). */
 const char* fc_strerror(int code);

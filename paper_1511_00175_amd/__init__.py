@@ -11,12 +11,12 @@ only marshals torch tensors (device memory and the current stream) into it.
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
                   FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
-                  fc_lr_at, fc_plan_read_timing, fc_plan_set_timing, fc_sgd_step, fc_step, fc_strerror, fc_train,
-                  fc_tree_reduce, lr_policy)
+                  fc_lr_at, fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks,
+                  fc_sgd_step, fc_step, fc_strerror, fc_train, fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
            "fc_plan_read_timing", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
-           "fc_lr_at", "fc_train", "lr_policy", "lr_at"]
+           "fc_lr_at", "fc_train", "lr_policy", "lr_at", "fc_read_probe", "fc_read_probe_blocks", "read_probe"]
 
 
 def lr_at(iter, batch, **policy):
@@ -25,6 +25,17 @@ def lr_at(iter, batch, **policy):
     if rc:
         raise FcError("fc_lr_at", rc)
     return lr
+
+def read_probe(src, out, stream=None):
+    """Streaming read of the whole tensor `src` (fc_read_probe); `out` is an
+    fp32 tensor of at least fc_read_probe_blocks(src bytes) elements."""
+    nbytes = src.numel() * src.element_size()
+    if out.numel() < fc_read_probe_blocks(nbytes):
+        raise ValueError("out is too small")
+    rc = fc_read_probe(src.data_ptr(), nbytes, out.data_ptr(), _stream(stream))
+    if rc:
+        raise FcError("fc_read_probe", rc)
+
 
 _DTYPES = {"f32": FC_F32, "f16": FC_F16}
 _ORDERS = {"tree": FC_ORDER_TREE, "linear": FC_ORDER_LINEAR}

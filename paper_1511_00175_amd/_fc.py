@@ -78,10 +78,14 @@ lib.fc_plan_query.argtypes = [_plan_p, ctypes.POINTER(fc_plan_info)]
 lib.fc_lr_at.argtypes = [ctypes.POINTER(fc_lr_policy), ctypes.c_int64, _i, ctypes.POINTER(ctypes.c_float)]
 lib.fc_train.argtypes = [_plan_p, _pp, _vp, _vp, ctypes.POINTER(fc_lr_policy), ctypes.c_int64, ctypes.c_int64,
                          _f, _f, _i, _vp]
+lib.fc_read_probe_blocks.argtypes = [ctypes.c_uint64]
+lib.fc_read_probe_blocks.restype = ctypes.c_uint64
+lib.fc_read_probe.argtypes = [_vp, ctypes.c_uint64, _vp, _vp]
 lib.fc_plan_set_timing.argtypes = [_plan_p, _i]
 lib.fc_plan_read_timing.argtypes = [_plan_p, ctypes.POINTER(fc_timing)]
 for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
-           "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing", "fc_lr_at", "fc_train"):
+           "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing", "fc_lr_at", "fc_train",
+           "fc_read_probe"):
     getattr(lib, _n).restype = ctypes.c_int
 
 
@@ -189,3 +193,11 @@ def fc_lr_at(policy, iter, batch):
 def fc_train(plan, grads, w, v, policy, first_iter, n_iters, mu, wd, batch, stream=0):
     return lib.fc_train(plan, _ptr_array(grads), w, v, ctypes.byref(policy), int(first_iter), int(n_iters),
                         mu, wd, int(batch), stream)
+
+
+def fc_read_probe_blocks(nbytes):
+    return lib.fc_read_probe_blocks(int(nbytes))
+
+
+def fc_read_probe(src, nbytes, out, stream=0):
+    return lib.fc_read_probe(src, int(nbytes), out, stream)

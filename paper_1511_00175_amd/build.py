@@ -6,6 +6,7 @@ Flags that matter for results:
   -Xclang -target-feature -Xclang -packed-fp32-ops: no packed fp32 ALU ops
 """
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -23,16 +24,38 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=
          "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+RESOURCES = os.path.join(PKG, "_build", "kernel_resources.txt")
+_REMARK = re.compile(r"remark:\s+(Function Name|VGPRs|AGPRs|ScratchSize \[bytes/lane\]|Occupancy \[waves/SIMD\]|"
+                     r"LDS Size \[bytes/block\]):\s+(\S+)")
+
+
+def _resources(stderr):
+    """Per-kernel resource usage from the compiler's kernel-resource-usage
+    remarks: {kernel: {field: value}}."""
+    out, cur = {}, None
+    for ln in stderr.splitlines():
+        m = _REMARK.search(ln)
+        if not m:
+            continue
+        key, val = m.group(1).split(" ")[0], m.group(2)
+        if key == "Function":
+            cur = out.setdefault(val, {})
+        elif cur is not None:
+            cur[key] = int(val)
+    return out
+
+
 def _compile(src, obj, extra):
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *FLAGS, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    remarks = ["-Rpass-analysis=kernel-resource-usage"] if src.endswith(".hip") else []
+    cmd = [HIPCC, *FLAGS, *remarks, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the packed-fp32 feature and says so; that is harmless
     noise = [ln for ln in r.stderr.splitlines() if ln.strip() and "packed-fp32-ops" not in ln
-             and "ignoring feature" not in ln]
+             and "ignoring feature" not in ln and "remark:" not in ln and "kernel-resource-usage" not in ln]
     if r.returncode:
         raise RuntimeError(f"hipcc failed for {src}:\n" + "\n".join(noise))
-    return obj
+    return _resources(r.stderr)
 
 
 def build(out=LIB, extra=()):
@@ -41,7 +64,16 @@ def build(out=LIB, extra=()):
     os.makedirs(objdir, exist_ok=True)
     objs = [os.path.join(objdir, s + ".o") for s in SOURCES]
     with ThreadPoolExecutor(len(SOURCES)) as ex:
-        list(ex.map(lambda a: _compile(*a, list(extra)), zip(SOURCES, objs)))
+        usage = {}
+        for u in ex.map(lambda a: _compile(*a, list(extra)), zip(SOURCES, objs)):
+            usage.update(u)
+    # every kernel keeps its reduction stack in registers: no scratch memory
+    with open(RESOURCES, "w") as f:
+        for name in sorted(usage):
+            f.write(name + " " + " ".join(f"{k}={v}" for k, v in sorted(usage[name].items())) + "\n")
+    spill = [n for n, u in usage.items() if u.get("ScratchSize", 0)]
+    if spill:
+        raise RuntimeError("kernels using scratch memory: " + ", ".join(spill))
     tmp = out + ".tmp"
     subprocess.run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp], check=True)
     os.replace(tmp, out)

@@ -293,7 +293,8 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
         delete p;
         return FC_EINVAL;
     }
-    sh.maxd = sh.kwaves == 1 ? need : fc::KSPLIT_MAXD;
+    // with a K split: the depth a wave's run of span / kchunk batches needs
+    sh.maxd = sh.kwaves == 1 ? need : bit_length(sh.span / sh.kchunk);
     p->shape = sh;
 
     // Tile map: each segment is cut into tiles of at most lanes*vecs vectors;
@@ -597,6 +598,16 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     rc = launch(p, FC_KERNEL_STEP, s, [&] { return launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
     note_stream(p, s);
     return rc;
+}
+
+uint64_t fc_read_probe_blocks(uint64_t bytes) { return fc::read_probe_blocks(bytes); }
+
+int fc_read_probe(const void* src, uint64_t bytes, float* out, void* stream) {
+    if (!src || !out || bytes == 0 || bytes % 16) return FC_EINVAL;
+    if (!aligned16(src) || (reinterpret_cast<uintptr_t>(out) & 3u)) return FC_EALIGN;
+    // one block per 16 KiB; the grid's x dimension is 32 bits
+    if (fc::read_probe_blocks(bytes) > 0x7fffffffu) return FC_EINVAL;
+    return hip_rc(fc::launch_read_probe(src, bytes, out, static_cast<hipStream_t>(stream)));
 }
 
 int fc_lr_at(const fc_lr_policy* pol, int64_t iter, int batch, float* lr) {

@@ -443,7 +443,7 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
 // finishes the tree that way.  Each wave streams 64*U contiguous vectors of
 // each of its replicas (4 KiB of fp32 for U = 4) while holding a stack for
 // only S leaves.
-template <int DT, int W, int V, int U, int C, int MODE>
+template <int DT, int W, int V, int U, int C, int D, int MODE>
 __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, uint64_t start, uint32_t count,
                                             float lr_j, float wd_j) {
     constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
@@ -462,7 +462,7 @@ __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, ui
             roff[u] = (vi < count ? vi : 0u) * V * SG;  // idle lanes re-read vector 0
         }
         Acc<U, V> x;
-        reduce<DT, V, U, C, KSPLIT_MAXD, true>(a.grads + q * S, q < nq ? S : r, start * SG, roff, x);
+        reduce<DT, V, U, C, D, true>(a.grads + q * S, q < nq ? S : r, start * SG, roff, x);
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -474,22 +474,19 @@ __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, ui
         // tile vector e = lane e % 64, vector e / 64: its partials sit at (q*U*64 + e)*V
         Acc<1, V> acc;
         if (nq == W && !r) {
-            // K = W * S: the W runs are the leaves of one balanced subtree; the
-            // combine's latency is exposed to the whole block, so keep it short
-            Acc<1, V> y[W];
+            // K = W * S: the W runs are the leaves of one balanced subtree.  The
+            // counter with constant indices has no selects (the combine's
+            // latency is exposed to the whole block) and holds log2(W) + 1
+            // partials instead of W.
+            Acc<1, V> st[DC];
 #pragma unroll
-            for (int n = 0; n < W; ++n)
+            for (int n = 0; n < W; ++n) {
+                Acc<1, V> p;
 #pragma unroll
-                for (int i = 0; i < V; ++i) y[n].a[0][i] = part[(n * U * WAVE + e) * V + i];
-#pragma unroll
-            for (int h = W / 2; h >= 1; h /= 2) {
-#pragma unroll
-                for (int m = 0; m < h; ++m) {
-                    add_right(y[2 * m], y[2 * m + 1]);
-                    if (m) set(y[m], y[2 * m]);
-                }
+                for (int i = 0; i < V; ++i) p.a[0][i] = part[(n * U * WAVE + e) * V + i];
+                push<DC>(st, p, n);
             }
-            set(acc, y[0]);
+            set(acc, st[DC - 1]);
         } else {
             Acc<1, V> st[DC];
             bool have = false;
@@ -526,8 +523,13 @@ __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, ui
     __syncthreads();  // the partials are overwritten by the block's next tile
 }
 
-template <int DT, int W, int U, int C, int MODE>
-__global__ __launch_bounds__(64 * W) void ksplit_kernel(ReduceArgs a) {
+// D: depth of each wave's pending-subtree stack (>= bit length of span / C).
+// The reduce-only kernel with U = 2 and C = 2 is held to 64 registers (8
+// waves per SIMD), so that two blocks of 16 waves share a CU and one block's
+// combine overlaps the other's loads (the fused variant would spill).
+template <int DT, int W, int U, int C, int D, int MODE>
+__global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ? 8 : 1) void ksplit_kernel(
+    ReduceArgs a) {
     __shared__ float part[W * U * 64 * 4];
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const Tile tile = ld_tile(a.tiles, t);
@@ -538,9 +540,9 @@ __global__ __launch_bounds__(64 * W) void ksplit_kernel(ReduceArgs a) {
             wd_j = a.wd * ldc(a.mults, 2 * j + 1);
         }
         if (!(tile.seg & TAIL_BIT))
-            ksplit_body<DT, W, 4, U, C, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
+            ksplit_body<DT, W, 4, U, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
         else
-            ksplit_body<DT, W, 1, 1, C, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
+            ksplit_body<DT, W, 1, 1, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
     }
 }
 
@@ -640,18 +642,20 @@ hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// (waves, lane vectors, replicas per batch) triples compiled for the K split.
+// (waves, lane vectors, replicas per batch) triples compiled for the K split,
+// each with a stack deep enough for runs of up to 8 batches.
 template <class F> hipError_t pick_ksplit(int w, int u, int c, F&& f) {
+    constexpr int D = KSPLIT_MAXD;
     if (u == 4 && c == 2) {
-        if (w == 4) return f(I<4>{}, I<4>{}, I<2>{});
-        if (w == 8) return f(I<8>{}, I<4>{}, I<2>{});
-        if (w == 16) return f(I<16>{}, I<4>{}, I<2>{});
+        if (w == 4) return f(I<4>{}, I<4>{}, I<2>{}, I<D>{});
+        if (w == 8) return f(I<8>{}, I<4>{}, I<2>{}, I<D>{});
+        if (w == 16) return f(I<16>{}, I<4>{}, I<2>{}, I<D>{});
     }
     if (u == 2 && c == 4) {
-        if (w == 8) return f(I<8>{}, I<2>{}, I<4>{});
-        if (w == 16) return f(I<16>{}, I<2>{}, I<4>{});
+        if (w == 8) return f(I<8>{}, I<2>{}, I<4>{}, I<D>{});
+        if (w == 16) return f(I<16>{}, I<2>{}, I<4>{}, I<D>{});
     }
-    if (u == 2 && c == 2 && w == 16) return f(I<16>{}, I<2>{}, I<2>{});
+    if (u == 2 && c == 2 && w == 16) return f(I<16>{}, I<2>{}, I<2>{}, I<D>{});
     return hipErrorInvalidValue;
 }
 
@@ -659,8 +663,8 @@ template <int DT>
 hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
     if (sh.kwaves > 1) {
         return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
-            return pick_ksplit(sh.kwaves, sh.vecs, sh.kchunk, [&](auto w, auto u, auto c) {
-                hipLaunchKernelGGL((ksplit_kernel<DT, w.value, u.value, c.value, md.value>), dim3(grid),
+            return pick_ksplit(sh.kwaves, sh.vecs, sh.kchunk, [&](auto w, auto u, auto c, auto d) {
+                hipLaunchKernelGGL((ksplit_kernel<DT, w.value, u.value, c.value, d.value, md.value>), dim3(grid),
                                    dim3(64 * w.value), 0, s, a);
                 return hipGetLastError();
             });

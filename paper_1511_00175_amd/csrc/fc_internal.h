@@ -76,9 +76,9 @@ struct BcastArgs {
 // instantiated); plans whose K / kchunk needs more are rejected at creation.
 constexpr int MAXD_MAX = 10;
 
-// K split across the waves of a block: the compiled (waves, lane vectors,
-// replicas per batch) triples, and the per-wave stack depth.  A wave's run of
-// `span` replicas takes at most KSPLIT_MAX_BATCHES batches of kchunk.
+// K split across the waves of a block: the deepest per-wave stack compiled.
+// A wave's run of `span` replicas takes at most KSPLIT_MAX_BATCHES batches of
+// kchunk.
 constexpr int KSPLIT_MAXD = 4;
 constexpr int KSPLIT_MAX_BATCHES = 8;
 
@@ -86,5 +86,7 @@ hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceAr
 hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s);
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s);
+uint64_t read_probe_blocks(uint64_t bytes);
+hipError_t launch_read_probe(const void* src, uint64_t bytes, float* out, hipStream_t s);
 
 }  // namespace fc

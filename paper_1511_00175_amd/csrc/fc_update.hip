@@ -22,4 +22,52 @@ hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream
     return pick<1, 2>(sh.vecs, go);
 }
 
+// Read probe: a plain streaming read of one contiguous buffer, the ceiling a
+// read-bound kernel can reach.  Each lane sums 4 vectors of 16 bytes (nt
+// loads); the wave and then the block add their lanes' sums and lane 0 of the
+// block stores one float, which keeps the loads live.  The value's rounding
+// order is not specified: it is a bandwidth probe, not a result.
+constexpr int PROBE_THREADS = 256;
+constexpr int PROBE_VECS = 4;
+
+__global__ __launch_bounds__(PROBE_THREADS) void read_probe_kernel(const void* src, uint64_t nvec, float* out) {
+    const uint64_t first = static_cast<uint64_t>(blockIdx.x) * PROBE_THREADS * PROBE_VECS;
+    const gptr_t base = gread(src) + first * 16;
+    f4 v[PROBE_VECS];
+#pragma unroll
+    for (int u = 0; u < PROBE_VECS; ++u) {
+        const uint64_t vi = first + threadIdx.x + u * PROBE_THREADS;
+        const uint32_t off = vi < nvec ? (threadIdx.x + u * PROBE_THREADS) * 16u : 0u;
+        v[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
+                                                                           CPOL_STREAM_LOAD));
+        if (vi >= nvec) v[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    float x = 0.0f;
+#pragma unroll
+    for (int u = 0; u < PROBE_VECS; ++u) x = x + ((v[u].x + v[u].y) + (v[u].z + v[u].w));
+#pragma unroll
+    for (int d = 32; d >= 1; d /= 2) x = x + __shfl_xor(x, d, 64);
+    __shared__ float wsum[PROBE_THREADS / 64];
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x / 64] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float t = 0.0f;
+#pragma unroll
+        for (int q = 0; q < PROBE_THREADS / 64; ++q) t = t + wsum[q];
+        out[blockIdx.x] = t;
+    }
+}
+
+uint64_t read_probe_blocks(uint64_t bytes) {
+    const uint64_t per = static_cast<uint64_t>(PROBE_THREADS) * PROBE_VECS * 16;
+    return (bytes + per - 1) / per;
+}
+
+hipError_t launch_read_probe(const void* src, uint64_t bytes, float* out, hipStream_t s) {
+    const uint64_t blocks = read_probe_blocks(bytes);
+    hipLaunchKernelGGL(read_probe_kernel, dim3(static_cast<unsigned>(blocks)), dim3(PROBE_THREADS), 0, s, src,
+                       bytes / 16, out);
+    return hipGetLastError();
+}
+
 }  // namespace fc

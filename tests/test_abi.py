@@ -108,3 +108,33 @@ def test_oracle_and_library_share_nothing():
     for fn in ("__init__.py", "_fc.py", "build.py"):
         text = open(os.path.join(ROOT, "paper_1511_00175_amd", fn)).read()
         assert "import oracle" not in text and "from oracle" not in text
+
+
+def test_kernels_use_no_scratch_memory():
+    """The build records the compiler's per-kernel resource usage: every
+    kernel keeps its pending-subtree stack and partial sums in registers and
+    LDS (no scratch memory), and the K-split kernels' LDS fits two blocks per
+    CU where it is meant to."""
+    path = os.path.join(ROOT, "paper_1511_00175_amd", "_build", "kernel_resources.txt")
+    if not os.path.exists(path):
+        pytest.skip("library not built by paper_1511_00175_amd/build.py")
+    rows = {}
+    with open(path) as f:
+        for line in f:
+            name, *kv = line.split()
+            rows[name] = dict(x.split("=") for x in kv)
+    assert len(rows) >= 100
+    assert all(r["ScratchSize"] == "0" for r in rows.values())
+    ks = [n for n in rows if "ksplit_kernel" in n]
+    assert ks and all(int(rows[n]["LDS"]) <= 65536 for n in ks)
+
+
+def test_read_probe_argument_errors(fcmod):
+    f = fcmod._fc
+    assert f.fc_read_probe(None, 16, 64, None) == f.FC_EINVAL
+    assert f.fc_read_probe(64, 16, None, None) == f.FC_EINVAL
+    assert f.fc_read_probe(64, 0, 64, None) == f.FC_EINVAL
+    assert f.fc_read_probe(64, 20, 64, None) == f.FC_EINVAL     # not a multiple of 16
+    assert f.fc_read_probe(72, 16, 64, None) == f.FC_EALIGN     # source not 16-byte aligned
+    assert f.fc_read_probe_blocks(1) == 1 and f.fc_read_probe_blocks(16384) == 1
+    assert f.fc_read_probe_blocks(16384 + 16) == 2

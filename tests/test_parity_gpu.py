@@ -10,7 +10,7 @@ operations in the same order with no contraction.
 import numpy as np
 import pytest
 
-from gpu_cases import run_reduce, run_steps, same_bits, to_dev
+from gpu_cases import LR, MU, WD, alloc_len, host_replicas, run_reduce, run_steps, same_bits, to_dev
 from workloads import gen
 
 pytestmark = pytest.mark.gpu
@@ -329,3 +329,54 @@ def test_empty_and_zero_length(fc):
     segs = [(0, 0, 1, 1), (8, 5, 1, 1), (16, 0, 1, 1)]
     bad, got, _ = run_reduce(fc, segs, 3, "f32", "tree", np.random.default_rng(1))
     assert bad == 0
+
+
+@pytest.mark.parametrize("K,dtype,schedule", [(4, "f32", 1), (130, "f32", 2), (16, "f16", 1), (128, "f32", 0)])
+def test_graph_capture_replays(fc, K, dtype, schedule):
+    """A step whose pointer tables are already on the device, called on the
+    stream it last ran on, enqueues kernel launches only, so it can be
+    captured in a HIP graph.  Every replay (with eager steps and
+    synchronizations in between) gives the bits of an eager twin plan."""
+    import torch
+    segs = table(13000 + K, dtype, nseg=4, max_len=3000)
+    n = alloc_len(segs)
+    rng = np.random.default_rng(K)
+    npdt = np.float16 if dtype == "f16" else np.float32
+    reps = to_dev(host_replicas(rng, K, n, npdt, scale=0.01))
+    w0 = (rng.standard_normal(n, dtype=np.float32) * np.float32(0.05))
+    wa, va = to_dev(w0), torch.zeros(n, device="cuda")
+    wb, vb = to_dev(w0), torch.zeros(n, device="cuda")
+    pa = fc.Plan(segs, K, dtype, "tree", schedule=schedule)
+    pb = fc.Plan(segs, K, dtype, "tree", schedule=schedule)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+    s.synchronize()
+    pb.step(reps, wb, vb, LR, MU, WD, 256)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+    for _ in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        pb.step(reps, wb, vb, LR, MU, WD, 256)
+        torch.cuda.synchronize()
+        assert same_bits(wa.cpu().numpy(), wb.cpu().numpy()) == 0
+        assert same_bits(va.cpu().numpy(), vb.cpu().numpy()) == 0
+    pa.close()
+    pb.close()
+
+
+def test_read_probe_reads_every_byte(fc):
+    """The probe's per-block sums of an all-ones buffer count its floats
+    exactly (a ragged last block included)."""
+    import torch
+    n = 3 * 4096 + 904
+    x = torch.ones(n, device="cuda")
+    blocks = fc.fc_read_probe_blocks(4 * n)
+    out = torch.full((blocks,), -1.0, device="cuda")
+    fc.read_probe(x, out)
+    torch.cuda.synchronize()
+    assert out.cpu().tolist() == [4096.0, 4096.0, 4096.0, 904.0]
