@@ -440,8 +440,8 @@ def main():
     achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
     plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE)
     traffic = read_traffic(wl.name, dom) if plain else None
-    sched = {1: "fused", 2: "two-pass"}.get(info.schedule, str(info.schedule))
-    rk = "ksplit_kernel" if info.k_waves > 1 else "reduce_kernel"
+    sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
+    rk = "ksplit_kernel" if info.k_waves > 1 else "resident_kernel" if info.schedule == 3 else "reduce_kernel"
 
     res = {
         "metric": METRIC,

@@ -88,13 +88,30 @@ typedef enum { FC_ORDER_TREE = 0, FC_ORDER_LINEAR = 1 } fc_order;
 
 typedef struct fc_plan fc_plan;
 
-/* How fc_step schedules the work.  FUSED: one kernel reads the replicas and
- * w, v and writes w', v'.  TWO_PASS: one kernel reduces into a raw-sum
- * buffer, a second applies the update (same bits; on MI355X this is faster
- * when the replicas dominate the bytes, because HBM serves a replica stream
- * with one write stream better than with two).  AUTO picks TWO_PASS when a
- * parameter's replicas take more than 256 bytes (K * bytes per element). */
-typedef enum { FC_SCHED_AUTO = 0, FC_SCHED_FUSED = 1, FC_SCHED_TWO_PASS = 2 } fc_schedule;
+/* How fc_step schedules the work (every schedule gives the same bits).
+ * FUSED: one kernel reads the replicas and w, v and writes w', v'.
+ * TWO_PASS: one kernel reduces into a raw-sum buffer, a second applies the
+ *   update (on MI355X faster than FUSED when the replicas dominate the bytes,
+ *   because HBM serves a replica stream with one write stream better than
+ *   with two).
+ * RESIDENT: one persistent launch, one block of 16 waves per compute unit;
+ *   each block first reduces its share of the parameters into LDS (HBM sees a
+ *   pure read stream) and then updates them from LDS, so the raw sum never
+ *   goes to HBM.  A block's share per round is what fits one compute unit's
+ *   LDS (1 KiB per 256-element tile: about 10 M parameters per round over 256
+ *   compute units of 160 KiB); larger plans take several rounds.  It also
+ *   makes fc_tree_reduce store the sums only after each read phase.  Uses the
+ *   tile shape (1 vector, 16 replicas, 64 lanes) and no K split.
+ * AUTO (no launch-shape field given): RESIDENT when one round holds the plan
+ *   or a parameter's replicas take at least 256 bytes (K * bytes per
+ *   element); otherwise TWO_PASS when they take more than 256 bytes, else
+ *   FUSED (with a launch-shape field: TWO_PASS or FUSED by that rule). */
+typedef enum {
+    FC_SCHED_AUTO = 0,
+    FC_SCHED_FUSED = 1,
+    FC_SCHED_TWO_PASS = 2,
+    FC_SCHED_RESIDENT = 3
+} fc_schedule;
 
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero selects the default, which depends on the
@@ -243,13 +260,15 @@ typedef struct {
     uint64_t n_elems;    /* sum of segment lengths */
     uint64_t extent;     /* one past the last segment element */
     int ntiles;          /* blocks of work in one launch */
-    int grid;            /* blocks launched */
-    int block_threads;
+    int grid;            /* blocks launched (RESIDENT: its persistent grid) */
+    int block_threads;   /* threads per block of the reduce or step launch */
     int vecs_per_thread;
     int kchunk;
-    int schedule;        /* resolved fc_schedule of fc_step: FUSED or TWO_PASS */
+    int schedule;        /* resolved fc_schedule of fc_step: FUSED, TWO_PASS or RESIDENT */
     uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
     int k_waves;         /* waves splitting the K replicas (1: no split) */
+    int lds_bytes;       /* RESIDENT: LDS per block (0 for the other schedules) */
+    int rounds;          /* RESIDENT: rounds of the persistent grid (0 otherwise) */
 } fc_plan_info;
 
 int fc_plan_query(const fc_plan* plan, fc_plan_info* info);

@@ -10,7 +10,7 @@ only marshals torch tensors (device memory and the current stream) into it.
 """
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
-                  FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
+                  FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
                   fc_lr_at, fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks,
                   fc_sgd_step, fc_step, fc_strerror, fc_train, fc_tree_reduce, lr_policy)
 
@@ -71,7 +71,7 @@ class Plan:
     order   : "tree" (reduction tree) or "linear" (parameter server).
     opts    : launch shape (block_threads, vecs_per_thread, kchunk,
               max_blocks, k_waves) and fc_step schedule (0 auto, 1 fused,
-              2 two-pass); results do not depend on them.
+              2 two-pass, 3 resident); results do not depend on them.
     """
 
     def __init__(self, segments, K, dtype="f32", order="tree", **opts):

@@ -31,10 +31,11 @@ class fc_plan_info(ctypes.Structure):
                 ("n_elems", ctypes.c_uint64), ("extent", ctypes.c_uint64), ("ntiles", ctypes.c_int),
                 ("grid", ctypes.c_int), ("block_threads", ctypes.c_int), ("vecs_per_thread", ctypes.c_int),
                 ("kchunk", ctypes.c_int), ("schedule", ctypes.c_int),
-                ("scratch_bytes", ctypes.c_uint64), ("k_waves", ctypes.c_int)]
+                ("scratch_bytes", ctypes.c_uint64), ("k_waves", ctypes.c_int), ("lds_bytes", ctypes.c_int),
+                ("rounds", ctypes.c_int)]
 
 
-FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS = 0, 1, 2
+FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS, FC_SCHED_RESIDENT = 0, 1, 2, 3
 FC_KERNEL_STEP, FC_KERNEL_REDUCE, FC_KERNEL_SGD, FC_KERNEL_BCAST, FC_KERNEL_KINDS = 0, 1, 2, 3, 4
 KERNEL_NAMES = ("step", "reduce", "sgd", "bcast")
 

@@ -37,6 +37,10 @@ struct fc_plan {
     float** d_dst = nullptr;         // K broadcast pointers
     float* d_sum = nullptr;          // raw-sum scratch of the two-pass schedule (extent floats)
     int schedule = FC_SCHED_FUSED;   // resolved schedule of fc_step
+    int* d_ranges = nullptr;         // RESIDENT: tile range of each block (res_grid + 1 entries)
+    int res_grid = 0;
+    int res_rounds = 0;
+    int res_lds = 0;                 // RESIDENT: LDS bytes per block
 
     // per-kernel timing (fc_plan_set_timing / fc_plan_read_timing)
     struct Rec {
@@ -118,21 +122,38 @@ hipError_t launch_reduce(const fc::Shape& sh, int mode, int grid, const fc::Redu
     return sh.dtype == FC_F16 ? fc::launch_reduce_f16(sh, mode, grid, a, s) : fc::launch_reduce_f32(sh, mode, grid, a, s);
 }
 
+hipError_t launch_resident(const fc_plan* p, int mode, const fc::ReduceArgs& r, hipStream_t s) {
+    fc::ResidentArgs a{};
+    a.r = r;
+    a.ranges = p->d_ranges;
+    a.rounds = p->res_rounds;
+    const size_t lds = static_cast<size_t>(p->res_lds);
+    return p->shape.dtype == FC_F16 ? fc::launch_resident_f16(p->shape, mode, p->res_grid, lds, a, s)
+                                    : fc::launch_resident_f32(p->shape, mode, p->res_grid, lds, a, s);
+}
+
 void note_stream(fc_plan* p, hipStream_t s) {
     p->last_stream = s;
     p->have_last_stream = true;
 }
 
 int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc_order order, int K, uint64_t n_elems,
-                  fc::Shape& sh) {
+                  fc::Shape& sh, bool& shape_given) {
     fc::default_shape(gdt, K, sh);
     int w = fc::default_kwaves(gdt, order, K, n_elems);
     int u = 4, c = 2;  // lane vectors and batch of a K split
+    shape_given = false;
     if (o) {
         if (o->k_waves < 0 || o->max_blocks < 0) return FC_EINVAL;
-        if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_TWO_PASS) return FC_EINVAL;
+        if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_RESIDENT) return FC_EINVAL;
         // an explicit shape without k_waves asks for the unsplit kernel
-        const bool shape_given = o->block_threads || o->vecs_per_thread || o->kchunk;
+        shape_given = o->block_threads || o->vecs_per_thread || o->kchunk || o->k_waves;
+        if (o->schedule == FC_SCHED_RESIDENT) {
+            // the resident kernel has one shape: 64 lanes, 1 vector, batches of 16
+            if (o->k_waves > 1 || (o->block_threads && o->block_threads != 64) ||
+                (o->vecs_per_thread && o->vecs_per_thread != 1) || (o->kchunk && o->kchunk != 16))
+                return FC_EINVAL;
+        }
         if (o->k_waves) w = o->k_waves;
         else if (shape_given) w = 1;
         if (w > 1) {
@@ -188,6 +209,7 @@ void free_plan(fc_plan* p) {
     }
     for (auto e : p->event_pool) (void)hipEventDestroy(e);
     if (p->d_sum) (void)hipFree(p->d_sum);
+    if (p->d_ranges) (void)hipFree(p->d_ranges);
     if (p->d_tiles) (void)hipFree(p->d_tiles);
     if (p->d_mults) (void)hipFree(p->d_mults);
     if (p->d_grads) (void)hipFree(p->d_grads);
@@ -274,8 +296,42 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     // byte offsets of every element must fit in 64 bits for every buffer
     if (end > (UINT64_MAX / 8)) return FC_EINVAL;
     fc::Shape sh{};
-    int rc = validate_opts(opts, gdt, order, K, n_elems, sh);
+    bool shape_given = false;
+    int rc = validate_opts(opts, gdt, order, K, n_elems, sh, shape_given);
     if (rc) return rc;
+    const int sched_req = opts ? opts->schedule : FC_SCHED_AUTO;
+
+    // RESIDENT: one block per compute unit; each round every block takes a
+    // range of 256-element tiles whose raw sums fit the compute unit's LDS
+    int device = 0, cus = 0, lds_cu = 0;
+    if (hipGetDevice(&device) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess)
+        return FC_EHIP;
+    uint64_t res_tiles = 0;
+    for (int j = 0; j < nseg; ++j)
+        res_tiles += (segs[j].length / vec + 63) / 64 + (segs[j].length % vec ? 1 : 0);
+    const uint64_t slot_bytes = fc::RESIDENT_SLOT * sizeof(float);
+    const uint64_t cap = std::max<uint64_t>(1, static_cast<uint64_t>(std::max(lds_cu, 0)) / slot_bytes);
+    int res_grid = std::max(1, cus);
+    if (opts && opts->max_blocks > 0) res_grid = std::min(res_grid, opts->max_blocks);
+    if (res_tiles > 0 && res_tiles < static_cast<uint64_t>(res_grid)) res_grid = static_cast<int>(res_tiles);
+    const uint64_t res_rounds = std::max<uint64_t>(1, (res_tiles + res_grid * cap - 1) / (res_grid * cap));
+    const uint64_t res_ranges = static_cast<uint64_t>(res_grid) * res_rounds;
+    const uint64_t res_lds = (res_tiles + res_ranges - 1) / res_ranges * slot_bytes;
+    if (res_ranges > static_cast<uint64_t>(INT32_MAX) - 1) return FC_EINVAL;
+    const bool resident =
+        sched_req == FC_SCHED_RESIDENT ||
+        (sched_req == FC_SCHED_AUTO && !shape_given &&
+         fc::default_resident(K, gdt == FC_F16 ? 2 : 4, static_cast<int64_t>(res_rounds)));
+    if (resident) {
+        sh.block = 64;
+        sh.vecs = 1;
+        sh.kchunk = 16;
+        sh.kwaves = 1;
+        sh.span = K;
+        sh.lanes = 64;
+    }
 
     fc_plan* p = new (std::nothrow) fc_plan();
     if (!p) return FC_ENOMEM;
@@ -341,20 +397,41 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     if (opts && opts->max_blocks > 0) grid = std::min(grid, opts->max_blocks);
     p->grid = grid;
 
-    // fc_step schedule: two passes when the replicas dominate the bytes (see fc_schedule)
-    const int sched = opts ? opts->schedule : FC_SCHED_AUTO;
-    p->schedule = sched == FC_SCHED_AUTO ? fc::default_schedule(K, p->sg) : sched;
-
-    if (hipGetDevice(&p->device) != hipSuccess) {
-        delete p;
-        return FC_EHIP;
+    // fc_step schedule (see fc_schedule)
+    if (resident) p->schedule = FC_SCHED_RESIDENT;
+    else p->schedule = sched_req == FC_SCHED_AUTO ? fc::default_schedule(K, p->sg) : sched_req;
+    p->device = device;
+    std::vector<int> ranges;
+    if (resident) {
+        p->res_grid = res_grid;
+        p->res_rounds = static_cast<int>(res_rounds);
+        p->res_lds = static_cast<int>(res_lds);
+        try {
+            ranges.resize(static_cast<size_t>(res_ranges) + 1);
+        } catch (const std::bad_alloc&) {
+            delete p;
+            return FC_ENOMEM;
+        }
+        // range i = [i * ntiles / R, (i + 1) * ntiles / R): at most ceil(ntiles / R) tiles
+        for (uint64_t i = 0; i <= res_ranges; ++i)
+            ranges[i] = static_cast<int>(static_cast<uint64_t>(p->ntiles) * i / res_ranges);
     }
+
     bool ok = hipMalloc(&p->d_tiles, std::max<size_t>(tiles.size(), 1) * sizeof(Tile)) == hipSuccess &&
               hipMalloc(&p->d_mults, mults.size() * sizeof(float)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_grads), K * sizeof(void*)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_dst), K * sizeof(float*)) == hipSuccess;
     if (ok && p->schedule == FC_SCHED_TWO_PASS && p->extent > 0)
         ok = hipMalloc(&p->d_sum, static_cast<size_t>(p->extent) * sizeof(float)) == hipSuccess;
+    if (ok && resident) {
+        ok = hipMalloc(reinterpret_cast<void**>(&p->d_ranges), ranges.size() * sizeof(int)) == hipSuccess &&
+             hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) == hipSuccess;
+        if (ok) {
+            const size_t lds = static_cast<size_t>(p->res_lds);
+            ok = (gdt == FC_F16 ? fc::prepare_resident_f16(sh, lds) : fc::prepare_resident_f32(sh, lds)) ==
+                 hipSuccess;
+        }
+    }
     if (ok && !tiles.empty())
         ok = hipMemcpy(p->d_tiles, tiles.data(), tiles.size() * sizeof(Tile), hipMemcpyHostToDevice) == hipSuccess;
     if (ok)
@@ -390,6 +467,13 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->schedule = p->schedule;
     info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
     info->k_waves = p->shape.kwaves;
+    info->lds_bytes = p->schedule == FC_SCHED_RESIDENT ? p->res_lds : 0;
+    info->rounds = p->schedule == FC_SCHED_RESIDENT ? p->res_rounds : 0;
+    if (p->schedule == FC_SCHED_RESIDENT) {
+        // the launch of fc_step and fc_tree_reduce: one block of 16 waves per compute unit
+        info->grid = p->res_grid;
+        info->block_threads = 64 * fc::RESIDENT_WAVES;
+    }
     return FC_OK;
 }
 
@@ -470,7 +554,10 @@ int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* strea
     a.K = p->K;
     a.span = p->shape.span;
     a.out = out;
-    rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s); });
+    rc = launch(p, FC_KERNEL_REDUCE, s, [&] {
+        return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_REDUCE, a, s)
+                                                : launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s);
+    });
     note_stream(p, s);
     return rc;
 }
@@ -595,7 +682,10 @@ int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, 
     a.mu = mu;
     a.wd = wd;
     a.c = c;
-    rc = launch(p, FC_KERNEL_STEP, s, [&] { return launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s); });
+    rc = launch(p, FC_KERNEL_STEP, s, [&] {
+        return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_STEP, a, s)
+                                                : launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s);
+    });
     note_stream(p, s);
     return rc;
 }

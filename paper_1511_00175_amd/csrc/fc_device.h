@@ -430,6 +430,28 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
     }
 }
 
+// The end of the work on one lane-vector whose raw sum s[0..V-1] is known:
+// reduce-only, store the sum; step, update w and v and store w', v' (and the
+// raw sum and the broadcast copies when asked for).
+template <int V, int MODE>
+__device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uint32_t off, const float* s,
+                                       float lr_j, float wd_j) {
+    if constexpr (MODE == MODE_REDUCE) {
+        st32r<V>(gwrite(a.out) + start4, off, s);
+    } else {
+        float w[V], v[V], wn[V], vn[V];
+        ld32s<V>(gread(a.w) + start4, off, w);
+        ld32s<V>(gread(a.v) + start4, off, v);
+#pragma unroll
+        for (int i = 0; i < V; ++i) sgd1(s[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
+        st32r<V>(gwrite(a.w) + start4, off, wn);
+        st32r<V>(gwrite(a.v) + start4, off, vn);
+        if (a.out) st32r<V>(gwrite(a.out) + start4, off, s);
+        if (a.dst)
+            for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
+    }
+}
+
 // ------------------------------------------------------------------ K split across waves
 // A block of W waves shares one tile of 64*U lane-vectors.  The K leaves are
 // cut into aligned runs of S = a.span leaves (a power of two, a multiple of
@@ -504,21 +526,7 @@ __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, ui
             fold<DC>(st, nq, acc, have);
         }
         if (static_cast<uint32_t>(e) >= count) continue;
-        const uint32_t off = static_cast<uint32_t>(e) * V * 4;
-        if constexpr (MODE == MODE_REDUCE) {
-            st32r<V>(gwrite(a.out) + start4, off, acc.a[0]);
-        } else {
-            float w[V], v[V], wn[V], vn[V];
-            ld32s<V>(gread(a.w) + start4, off, w);
-            ld32s<V>(gread(a.v) + start4, off, v);
-#pragma unroll
-            for (int i = 0; i < V; ++i) sgd1(acc.a[0][i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
-            st32r<V>(gwrite(a.w) + start4, off, wn);
-            st32r<V>(gwrite(a.v) + start4, off, vn);
-            if (a.out) st32r<V>(gwrite(a.out) + start4, off, acc.a[0]);
-            if (a.dst)
-                for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
-        }
+        finish<V, MODE>(a, start4, static_cast<uint32_t>(e) * V * 4, acc.a[0], lr_j, wd_j);
     }
     __syncthreads();  // the partials are overwritten by the block's next tile
 }
@@ -543,6 +551,66 @@ __global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ?
             ksplit_body<DT, W, 4, U, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
         else
             ksplit_body<DT, W, 1, 1, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
+    }
+}
+
+// ------------------------------------------------------------------ resident step
+// One persistent block per CU, for each of the plan's rounds.  Phase 1: wave
+// q of the block reduces tiles lo + q, lo + q + W, ... of its range exactly
+// as reduce_kernel does (same loads, same association) and parks the raw
+// sums in the tile's LDS slot; HBM sees a pure read stream, no writes.
+// Phase 2, after a barrier: the block's threads walk the range again, one
+// wave per tile, and finish each lane-vector from LDS (the SGD update, or
+// the store of the raw sum).  In round r the blocks' ranges are neighbours,
+// so the whole grid streams one region of the parameters at a time.  Blocks
+// share nothing, so the result does not depend on how many of them are
+// resident at once.
+template <int DT, int W, int C, int MAXD, bool TREE, int MODE>
+__global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
+    extern __shared__ float slots[];
+    const ReduceArgs& a = ra.r;
+    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
+    const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const uint32_t lane = threadIdx.x & 63;
+    for (int round = 0; round < ra.rounds; ++round) {
+        const int b = static_cast<int>(blockIdx.x) + round * static_cast<int>(gridDim.x);
+        const int lo = ldc(ra.ranges, b);
+        const int hi = ldc(ra.ranges, b + 1);
+        for (int t = lo + q; t < hi; t += W) {
+            const Tile tile = ld_tile(a.tiles, t);
+            float* slot = slots + (t - lo) * RESIDENT_SLOT;
+            const uint32_t vi = lane < tile.count ? lane : 0u;  // idle lanes re-read the first vector
+            if (!(tile.seg & TAIL_BIT)) {
+                const uint32_t off[1] = {vi * 4 * SG};
+                Acc<1, 4> x;
+                reduce<DT, 4, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) slot[lane * 4 + i] = x.a[0][i];
+            } else {
+                const uint32_t off[1] = {vi * SG};
+                Acc<1, 1> x;
+                reduce<DT, 1, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+                slot[lane] = x.a[0][0];
+            }
+        }
+        __syncthreads();
+        const int n = (hi - lo) * 64;
+        for (int e = static_cast<int>(threadIdx.x); e < n; e += 64 * W) {
+            const int j = __builtin_amdgcn_readfirstlane(e / 64);  // one tile per wave
+            const Tile tile = ld_tile(a.tiles, lo + j);
+            if (lane >= tile.count) continue;
+            float lr_j = 0.0f, wd_j = 0.0f;
+            if constexpr (MODE == MODE_STEP) {
+                const int sj = static_cast<int>(tile.seg & SEG_MASK);
+                lr_j = a.lr * ldc(a.mults, 2 * sj);
+                wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
+            }
+            const float* slot = slots + j * RESIDENT_SLOT;
+            const uint64_t start4 = tile.start * 4;
+            if (!(tile.seg & TAIL_BIT)) finish<4, MODE>(a, start4, lane * 16, slot + lane * 4, lr_j, wd_j);
+            else finish<1, MODE>(a, start4, lane * 4, slot + lane, lr_j, wd_j);
+        }
+        __syncthreads();  // the next round's phase 1 overwrites the slots
     }
 }
 
@@ -679,6 +747,40 @@ hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArg
             }
             return go_reduce<DT, 0, md.value, u.value, c.value, 1>(grid, sh.block, a, s);
         });
+    });
+}
+
+// The resident kernel instance for a plan's shape: f(kernel instance tag).
+template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F&& f) {
+    if (sh.vecs != 1 || sh.kchunk != 16 || sh.block != 64) return hipErrorInvalidValue;
+    return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
+        return pick_maxd(sh.maxd, [&](auto d) {
+            if (sh.tree) return f(&resident_kernel<DT, RESIDENT_WAVES, 16, d.value, true, md.value>);
+            return f(&resident_kernel<DT, RESIDENT_WAVES, 16, d.value, false, md.value>);
+        });
+    });
+}
+
+// Allow `lds` bytes of dynamic LDS for the plan's resident kernels (both
+// modes), on the current device; called once when a plan is created.
+template <int DT>
+hipError_t prepare_resident_dt(const Shape& sh, size_t lds) {
+    for (int mode : {static_cast<int>(MODE_REDUCE), static_cast<int>(MODE_STEP)}) {
+        const hipError_t e = pick_resident<DT>(sh, mode, [&](auto kernel) {
+            return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        });
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <int DT>
+hipError_t launch_resident_dt(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a,
+                              hipStream_t s) {
+    return pick_resident<DT>(sh, mode, [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(grid), dim3(64 * RESIDENT_WAVES), lds, s, a);
+        return hipGetLastError();
     });
 }
 

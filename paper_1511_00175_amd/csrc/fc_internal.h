@@ -52,6 +52,19 @@ struct ReduceArgs {
     float lr, mu, wd, c;          // c = 1.0f / (float)batch
 };
 
+// The whole step in one persistent launch with the raw sums held in LDS:
+// the tile map (256-element tiles: 64 lanes of one 4-element vector) is cut
+// into gridDim.x * rounds contiguous ranges; in round r block b owns tiles
+// [ranges[b + r * gridDim.x], ranges[b + r * gridDim.x + 1]) and reserves
+// RESIDENT_SLOT floats of LDS per tile.
+struct ResidentArgs {
+    ReduceArgs r;
+    const int* ranges;            // gridDim.x * rounds + 1 tile indices
+    int rounds;
+};
+constexpr int RESIDENT_SLOT = 256;
+constexpr int RESIDENT_WAVES = 16;
+
 struct SgdArgs {
     const Tile* tiles;
     int ntiles;
@@ -86,6 +99,10 @@ hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceAr
 hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s);
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s);
+hipError_t prepare_resident_f32(const Shape& sh, size_t lds);
+hipError_t prepare_resident_f16(const Shape& sh, size_t lds);
+hipError_t launch_resident_f32(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a, hipStream_t s);
+hipError_t launch_resident_f16(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a, hipStream_t s);
 uint64_t read_probe_blocks(uint64_t bytes);
 hipError_t launch_read_probe(const void* src, uint64_t bytes, float* out, hipStream_t s);
 

@@ -7,4 +7,11 @@ hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceAr
     return launch_reduce_dt<FC_F16>(sh, mode, grid, a, s);
 }
 
+hipError_t launch_resident_f16(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a,
+                               hipStream_t s) {
+    return launch_resident_dt<FC_F16>(sh, mode, grid, lds, a, s);
+}
+
+hipError_t prepare_resident_f16(const Shape& sh, size_t lds) { return prepare_resident_dt<FC_F16>(sh, lds); }
+
 }  // namespace fc

@@ -59,6 +59,16 @@ inline bool compiled_pair(int u, int c) {
            (u == 4 && (c == 2 || c == 4 || c == 8));
 }
 
+// The resident schedule (sums parked in LDS, one persistent launch) when one
+// round of the grid holds the whole plan, or when a parameter's replicas take
+// at least 256 bytes.  Measured on MI355X: GoogLeNet K=128 543 us vs 574
+// (two passes), NiN K=32 162 vs 175 (fused), AlexNet fp16 K=128 in 24 rounds
+// 2548 vs 2680 (fused); VGG-19 K=16 in 14 rounds 2056 vs 1955 (K split,
+// fused), where w and v are a fifth of the bytes.
+inline bool default_resident(int K, int bytes_per_element, int64_t rounds) {
+    return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 256;
+}
+
 // Two passes (reduce into a raw-sum buffer, then update) when a parameter's
 // replicas take more than 256 bytes: HBM serves the replica stream with one
 // write stream far better than with two (measured on MI355X; see fc_schedule).

@@ -58,7 +58,11 @@ def test_strerror(fcmod):
     ([(0, 16)], 4, 0, {"vecs_per_thread": 1, "kchunk": 4}, -1),   # pair not compiled
     ([(0, 16)], 4, 0, {"vecs_per_thread": 4, "kchunk": 16}, -1),
     ([(0, 16)], 4, 0, {"max_blocks": -1}, -1),
-    ([(0, 16)], 4, 0, {"schedule": 3}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 4}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 3, "k_waves": 4}, -1),        # resident: one launch shape
+    ([(0, 16)], 4, 0, {"schedule": 3, "vecs_per_thread": 4}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 3, "block_threads": 128}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 3, "kchunk": 8}, -1),
 ])
 def test_plan_argument_errors(fcmod, segs, K, gdt, opts, code):
     rc, h = fcmod._fc.fc_plan_create(segs, K, gdt, 0, opts)

@@ -103,6 +103,7 @@ PAIRS = [(1, 8), (1, 16), (2, 8), (2, 16), (4, 2), (4, 4), (4, 8)]
 SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c) for b in (64, 128, 256) for u, c in PAIRS]
 SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, kchunk=8, max_blocks=5)]
 SHAPES += [dict(k_waves=8), dict(k_waves=16), dict(k_waves=16, schedule=2), dict(k_waves=8, max_blocks=3)]
+SHAPES += [dict(schedule=3), dict(schedule=3, max_blocks=7), dict(schedule=3, max_blocks=1)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -184,7 +185,7 @@ def test_ksplit_default_rule(fc):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("schedule", [1, 2])
+@pytest.mark.parametrize("schedule", [1, 2, 3])
 @pytest.mark.parametrize("K", [3, 64, 130])
 def test_schedules_match_oracle(fc, K, schedule, dtype):
     """fc_step in one fused pass and in two passes (raw sum, then update),
@@ -197,14 +198,45 @@ def test_schedules_match_oracle(fc, K, schedule, dtype):
 
 
 def test_schedule_resolution(fc):
-    """AUTO takes two passes when a parameter's replicas exceed 256 bytes;
-    only then does the plan own a raw-sum scratch buffer."""
-    segs = [(0, 1000, 1, 1), (1024, 5, 1, 1)]
+    """AUTO takes the resident schedule when every block's share of tiles
+    fits a compute unit's LDS; otherwise two passes when a parameter's
+    replicas exceed 256 bytes, only then with a raw-sum scratch buffer."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    small = [(0, 1000, 1, 1), (1024, 5, 1, 1)]
+    for K, dtype in ((1, "f32"), (64, "f32"), (1024, "f32"), (129, "f16")):
+        info = fc.Plan(small, K, dtype, "tree").info()
+        assert (info.schedule, info.scratch_bytes, info.rounds) == (3, 0, 1), (K, dtype)
+        assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
+        # 3 tiles of 256 elements and one of 232, then the 5-element segment's
+        # vector and its tail tile: one tile per block, 1 KiB of LDS each
+        assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 1024)
+    # 160 tiles per block fill 160 KiB of LDS: 256-element tiles for cus * 160 tiles fit
+    fits = [(0, cus * 160 * 256, 1, 1)]
+    big = [(0, cus * 160 * 256 + 4, 1, 1)]
+    info = fc.Plan(fits, 8, "f32", "tree").info()
+    assert (info.schedule, info.rounds, info.lds_bytes, info.grid) == (3, 1, 160 * 1024, cus)
     for K, dtype, two in ((64, "f32", False), (65, "f32", True), (128, "f16", False), (129, "f16", True)):
-        info = fc.Plan(segs, K, dtype, "tree").info()
+        p = fc.Plan(big, K, dtype, "tree", k_waves=1)
+        info = p.info()
         assert info.schedule == (2 if two else 1), (K, dtype)
-        assert info.scratch_bytes == (4 * 1029 if two else 0)
-    assert fc.Plan(segs, 128, "f32", "tree", schedule=1).info().scratch_bytes == 0
+        assert info.scratch_bytes == (4 * big[0][1] if two else 0)
+        p.close()
+    # without a launch shape, plans of several rounds are resident when a
+    # parameter's replicas take at least 256 bytes
+    for K, dtype, sched in ((63, "f32", 1), (64, "f32", 3), (127, "f16", 1), (128, "f16", 3)):
+        p = fc.Plan(big, K, dtype, "tree")
+        assert p.info().schedule == sched, (K, dtype)
+        p.close()
+    assert fc.Plan(small, 128, "f32", "tree", schedule=1).info().scratch_bytes == 0
+    # an explicit launch shape keeps AUTO off the resident kernel; a plan that
+    # needs more than one round is resident only when asked for
+    assert fc.Plan(small, 8, "f32", "tree", block_threads=64).info().schedule == 1
+    assert fc.Plan(big, 8, "f32", "tree").info().schedule == 1
+    assert fc.Plan(big, 64, "f32", "tree", block_threads=64).info().schedule == 1
+    info = fc.Plan(big, 8, "f32", "tree", schedule=3).info()
+    assert (info.schedule, info.rounds) == (3, 2)
+    assert info.lds_bytes == (cus * 160 + 1 + 2 * cus - 1) // (2 * cus) * 1024
 
 
 def test_timing_records_every_launch(fc):
@@ -213,14 +245,14 @@ def test_timing_records_every_launch(fc):
     K = 130
     reps = torch.randn((K, 5120), device="cuda")
     w, v, g = (torch.zeros(5120, device="cuda") for _ in range(3))
-    for schedule in (1, 2):
+    for schedule in (1, 2, 3):
         plan = fc.Plan(segs, K, "f32", "tree", schedule=schedule)
         plan.set_timing(True)
         for _ in range(3):
             plan.step(reps, w, v, 0.1, 0.9, 0.0, 64)
         plan.tree_reduce(reps, g)
         t = plan.read_timing()
-        if schedule == 1:
+        if schedule in (1, 3):
             assert t["step"][0] == 3 and t["reduce"][0] == 1 and t["sgd"][0] == 0
         else:
             assert t["step"][0] == 0 and t["reduce"][0] == 4 and t["sgd"][0] == 3
@@ -380,3 +412,37 @@ def test_read_probe_reads_every_byte(fc):
     fc.read_probe(x, out)
     torch.cuda.synchronize()
     assert out.cpu().tolist() == [4096.0, 4096.0, 4096.0, 904.0]
+
+
+@pytest.mark.parametrize("order", ["tree", "linear"])
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("K,max_blocks", [(1, 0), (17, 0), (100, 3), (1024, 0), (33, 1)])
+def test_resident_matches_oracle(fc, K, max_blocks, dtype, order):
+    """The resident schedule (phase 1: reduce each block's tiles into LDS;
+    phase 2: finish them from LDS): reduce and steps with raw sum and
+    broadcast, blocks with one tile or with many, both orders."""
+    segs = table(14000 + K, dtype, nseg=5, max_len=3000 if K < 1000 else 800)
+    rng = np.random.default_rng(K + 3)
+    opts = dict(schedule=3, max_blocks=max_blocks)
+    bad, _, _ = run_reduce(fc, segs, K, dtype, order, rng, opts=opts)
+    assert bad == 0
+    assert run_steps(fc, segs, K, dtype, order, rng, steps=2, opts=opts, with_out=True,
+                     with_bcast=K <= 17) == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("K,max_blocks", [(5, 1), (33, 2), (130, 1)])
+def test_resident_rounds_match_oracle(fc, K, max_blocks, dtype):
+    """A plan larger than the grid's LDS takes several rounds (here with 1-3
+    blocks of 160 tile slots each); every round's ranges are finished before
+    the next round's reduce reuses the slots."""
+    rows = [(0, 50000, 1, 1), (50048, 7, 2.0, 0.0), (50112, 60001, 1, 1)]
+    p = fc.Plan(rows, K, dtype, "tree", schedule=3, max_blocks=max_blocks)
+    info = p.info()
+    p.close()
+    assert info.rounds >= 2 and info.grid == max_blocks
+    rng = np.random.default_rng(K)
+    opts = dict(schedule=3, max_blocks=max_blocks)
+    bad, _, _ = run_reduce(fc, rows, K, dtype, "tree", rng, opts=opts)
+    assert bad == 0
+    assert run_steps(fc, rows, K, dtype, "tree", rng, steps=2, opts=opts, with_out=True) == 0

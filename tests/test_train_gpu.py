@@ -22,9 +22,10 @@ POLICIES = [dict(kind="step", base_lr=0.01, gamma=0.1, stepsize=10, base_batch=2
             dict(kind="fixed", base_lr=0.04)]
 
 
-@pytest.mark.parametrize("K,dtype", [(5, "f32"), (70, "f32"), (9, "f16")])
+# K, replica type, fc_step schedule (fused, two passes, resident)
+@pytest.mark.parametrize("K,dtype,schedule", [(5, "f32", 1), (70, "f32", 2), (9, "f16", 3), (33, "f32", 3)])
 @pytest.mark.parametrize("pi", range(len(POLICIES)))
-def test_train_matches_oracle(fc, K, dtype, pi):
+def test_train_matches_oracle(fc, K, dtype, schedule, pi):
     import torch
     pol = POLICIES[pi]
     rng = np.random.default_rng(K * 10 + pi)
@@ -35,7 +36,7 @@ def test_train_matches_oracle(fc, K, dtype, pi):
     v = np.zeros(n, np.float32)
     batch = 1024
     ew, ev = oracle.train(rows, list(reps), w, v, 0.9, 5e-4, batch, range(40), pol)
-    plan = fc.Plan(rows, K, dtype, "tree")
+    plan = fc.Plan(rows, K, dtype, "tree", schedule=schedule)
     w_d, v_d = to_dev(w), to_dev(v)
     r_d = to_dev(reps)
     plan.train(r_d, w_d, v_d, pol, 0, 25, 0.9, 5e-4, batch)   # iterations 0..24
