@@ -11,9 +11,10 @@ previous step's cache lines.
 
 Prints ONE JSON line: effective HBM GB/s of the step (algorithmic bytes per
 step / wall time per step over the timed steps), the roofline entry of the
-dominant kernel (its algorithmic bytes per launch / its average duration from
-HIP events the library records on the launch stream, against the 8 TB/s HBM3E
-peak), and the oracle timed on one host core as a CPU baseline.
+dominant kernel (its algorithmic bytes per step / its time per step from HIP
+events the library records on the launch stream around each call, all of the
+call's launches included, against the 8 TB/s HBM3E peak), and the oracle
+timed on the host cores as a CPU baseline.
 
     python bench.py [--workload googlenet] [--steps 200] [--warmup 20]
 """
@@ -70,9 +71,9 @@ def kernel_bytes(wl, kind, out=False, bcast=False):
 
 
 def read_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary for this workload, or None when absent or taken on another
-    version of the library sources."""
+    """HBM bytes per step moved by `kernel` (all its launches in one step)
+    from the committed rocprofv3 counter summary for this workload, or None
+    when absent or taken on another version of the library sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -85,7 +86,7 @@ def read_traffic(workload, kernel):
     if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("kernel") != kernel:
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv["hbm_bytes_per_step"])
     except (KeyError, ValueError):
         return None
 
@@ -466,7 +467,7 @@ def main():
             "algorithmic_bytes_per_step": bytes_step,
             "launch": {"grid": info.grid, "tiles": info.ntiles, "block_threads": info.block_threads,
                        "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "k_waves": info.k_waves,
-                       "schedule": sched},
+                       "schedule": sched, "rounds": info.rounds, "lds_bytes": info.lds_bytes},
             "input_sets": args.rotate,
             "kernels": kernels,
             "parallelism": "single GPU",

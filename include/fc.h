@@ -99,13 +99,14 @@ typedef struct fc_plan fc_plan;
  *   pure read stream) and then updates them from LDS, so the raw sum never
  *   goes to HBM.  A block's share per round is what fits one compute unit's
  *   LDS (1 KiB per 256-element tile: about 10 M parameters per round over 256
- *   compute units of 160 KiB); larger plans take several rounds.  It also
+ *   compute units of 160 KiB); larger plans take several rounds, one launch
+ *   per round.  It also
  *   makes fc_tree_reduce store the sums only after each read phase.  Uses the
  *   tile shape (1 vector, 16 replicas, 64 lanes) and no K split.
  * AUTO (no launch-shape field given): RESIDENT when one round holds the plan
- *   or a parameter's replicas take at least 256 bytes (K * bytes per
- *   element); otherwise TWO_PASS when they take more than 256 bytes, else
- *   FUSED (with a launch-shape field: TWO_PASS or FUSED by that rule). */
+ *   or a parameter's replicas take at least 64 bytes (K * bytes per element),
+ *   else FUSED.  With a launch-shape field: TWO_PASS when they take more than
+ *   256 bytes, else FUSED. */
 typedef enum {
     FC_SCHED_AUTO = 0,
     FC_SCHED_FUSED = 1,
@@ -115,9 +116,10 @@ typedef enum {
 
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero selects the default, which depends on the
- * replica type, K and the plan's size (measured on MI355X): fp32 in tree order
- * with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8 waves (see
- * k_waves); otherwise fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
+ * schedule, the replica type, K and the plan's size (measured on MI355X):
+ * RESIDENT -> (1 vector, 16 replicas, 64-lane tiles); otherwise fp32 in tree
+ * order with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8
+ * waves (see k_waves); fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
  * 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads
  * always carry the streaming (nt) hint. */
 typedef struct {

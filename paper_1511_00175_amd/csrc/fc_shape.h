@@ -18,8 +18,9 @@ namespace fc {
 // Four vectors per lane make every wave read 4 KiB of one replica at a time,
 // which HBM serves better than 1 KiB pieces, as long as the lane's registers
 // (16 accumulators per pending subtree) still allow enough waves in flight.
-// K split across waves by default (8 waves, 4 vectors per lane, 2 replicas
-// per batch, fused step) for fp32 replicas in tree order with 16 <= K <= 48
+// K split across waves by default in the fused and two-pass schedules (8
+// waves, 4 vectors per lane, 2 replicas per batch) for fp32 replicas in tree
+// order with 16 <= K <= 48
 // when w and v (8 bytes per parameter) exceed the 256 MiB Infinity Cache:
 // measured on MI355X, VGG-19-sized plans gain 5-12% at K = 16..32 and
 // AlexNet-sized fp32 plans 2-4%, while plans whose w, v stay cache-resident
@@ -59,14 +60,17 @@ inline bool compiled_pair(int u, int c) {
            (u == 4 && (c == 2 || c == 4 || c == 8));
 }
 
-// The resident schedule (sums parked in LDS, one persistent launch) when one
-// round of the grid holds the whole plan, or when a parameter's replicas take
-// at least 256 bytes.  Measured on MI355X: GoogLeNet K=128 543 us vs 574
-// (two passes), NiN K=32 162 vs 175 (fused), AlexNet fp16 K=128 in 24 rounds
-// 2548 vs 2680 (fused); VGG-19 K=16 in 14 rounds 2056 vs 1955 (K split,
-// fused), where w and v are a fifth of the bytes.
+// The resident schedule (sums parked in LDS, one persistent grid, one launch
+// per round) when one round of the grid holds the whole plan, or when a
+// parameter's replicas take at least 64 bytes.  Measured on MI355X (us per
+// step, resident vs the best other schedule): GoogLeNet K=128 543 vs 574,
+// NiN K=32 162 vs 175, VGG-19 K=16 1926 vs 1979 and K=32 3323 vs 3567 (14
+// rounds), AlexNet fp16 K=32/64/128 814/1379/2574 vs 890/1535/2579 and fp32
+// K=32/64 1431/2553 vs 1473/2810 (6 rounds); below 64 bytes the fused kernel
+// wins (VGG-19 K=8 1213 vs 1203, K=4 846 vs 766; AlexNet fp16 K=16 521 vs
+// 517), its update writes being a larger share of the bytes.
 inline bool default_resident(int K, int bytes_per_element, int64_t rounds) {
-    return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 256;
+    return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 64;
 }
 
 // Two passes (reduce into a raw-sum buffer, then update) when a parameter's

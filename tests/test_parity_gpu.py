@@ -171,17 +171,21 @@ def test_ksplit_plan_info(fc):
 
 
 def test_ksplit_default_rule(fc):
-    """The split is the default only for fp32 tree plans with 16 <= K <= 48
-    and at least 2^25 parameters."""
+    """In the fused schedule the split is the default only for fp32 tree
+    plans with 16 <= K <= 48 and at least 2^25 parameters (without a schedule
+    such plans are resident)."""
     big = [(0, 1 << 25, 1, 1)]
     small = [(0, (1 << 25) - 4, 1, 1)]
     for segs, K, dtype, order, kw in ((big, 16, "f32", "tree", 8), (big, 48, "f32", "tree", 8),
                                       (big, 15, "f32", "tree", 1), (big, 49, "f32", "tree", 1),
                                       (big, 16, "f32", "linear", 1), (big, 16, "f16", "tree", 1),
                                       (small, 16, "f32", "tree", 1)):
-        p = fc.Plan(segs, K, dtype, order)
+        p = fc.Plan(segs, K, dtype, order, schedule=1)
         assert p.info().k_waves == kw, (K, dtype, order, len(segs))
         p.close()
+    p = fc.Plan(big, 16, "f32", "tree")
+    assert (p.info().schedule, p.info().k_waves) == (3, 1)
+    p.close()
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -223,8 +227,8 @@ def test_schedule_resolution(fc):
         assert info.scratch_bytes == (4 * big[0][1] if two else 0)
         p.close()
     # without a launch shape, plans of several rounds are resident when a
-    # parameter's replicas take at least 256 bytes
-    for K, dtype, sched in ((63, "f32", 1), (64, "f32", 3), (127, "f16", 1), (128, "f16", 3)):
+    # parameter's replicas take at least 64 bytes
+    for K, dtype, sched in ((15, "f32", 1), (16, "f32", 3), (31, "f16", 1), (32, "f16", 3), (130, "f32", 3)):
         p = fc.Plan(big, K, dtype, "tree")
         assert p.info().schedule == sched, (K, dtype)
         p.close()
@@ -234,6 +238,7 @@ def test_schedule_resolution(fc):
     assert fc.Plan(small, 8, "f32", "tree", block_threads=64).info().schedule == 1
     assert fc.Plan(big, 8, "f32", "tree").info().schedule == 1
     assert fc.Plan(big, 64, "f32", "tree", block_threads=64).info().schedule == 1
+    assert fc.Plan(big, 65, "f32", "tree", block_threads=64).info().schedule == 2
     info = fc.Plan(big, 8, "f32", "tree", schedule=3).info()
     assert (info.schedule, info.rounds) == (3, 2)
     assert info.lds_bytes == (cus * 160 + 1 + 2 * cus - 1) // (2 * cus) * 1024
