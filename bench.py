@@ -236,6 +236,21 @@ def sweep_k(args):
                               "bound_gamma_d": d * u / (1 - d * u)}), flush=True)
 
 
+def input_hash(sets):
+    """sha256 (first 16 hex digits) over the first and last 4 KiB of every
+    input buffer (each replica row, w, v) of every input set, in order: names
+    the synthetic inputs a run measured."""
+    import torch
+
+    h = hashlib.sha256()
+    for reps, w, v in sets:
+        for t in [reps[k] for k in range(reps.shape[0])] + [w, v]:
+            b = t.view(-1).view(dtype=torch.uint8)
+            h.update(b[:4096].cpu().numpy().tobytes())
+            h.update(b[-4096:].cpu().numpy().tobytes())
+    return h.hexdigest()[:16]
+
+
 def graph_steps(plan, wl, inputs, out, bcast, n):
     """Capture n consecutive steps on one input set in one HIP graph (the
     plan's device tables already hold these pointers, so the captured calls
@@ -411,6 +426,19 @@ def main():
                 n0, us0 = timing.get(k, (0, 0.0))
                 timing[k] = (n0 + n, us0 + us)
             p.set_timing(False)
+    # timed region 3: one pair of torch events around every step (the library
+    # launches on torch's current stream), for the median and spread
+    per_step = []
+    for _ in range(max(50, min(args.steps, 200))):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        step()
+        e1.record()
+        per_step.append((e0, e1))
+    torch.cuda.synchronize()
+    step_us = sorted(a.elapsed_time(b) * 1e3 for a, b in per_step)
+    step_times = {"events": len(step_us), "median_us": round(step_us[len(step_us) // 2], 2),
+                  "p10_us": round(step_us[len(step_us) // 10], 2), "p90_us": round(step_us[len(step_us) * 9 // 10], 2)}
     graph = None
     if args.graph > 0:
         graph = graph_steps(plan, wl, sets[0], out, bcast, args.graph)
@@ -469,6 +497,8 @@ def main():
                        "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "k_waves": info.k_waves,
                        "schedule": sched, "rounds": info.rounds, "lds_bytes": info.lds_bytes},
             "input_sets": args.rotate,
+            "input_hash": input_hash(sets),
+            "step_times": step_times,
             "kernels": kernels,
             "parallelism": "single GPU",
         },

@@ -368,14 +368,17 @@ def test_empty_and_zero_length(fc):
     assert bad == 0
 
 
-@pytest.mark.parametrize("K,dtype,schedule", [(4, "f32", 1), (130, "f32", 2), (16, "f16", 1), (128, "f32", 0)])
-def test_graph_capture_replays(fc, K, dtype, schedule):
+@pytest.mark.parametrize("K,dtype,schedule,max_blocks", [(4, "f32", 1, 0), (130, "f32", 2, 0), (16, "f16", 1, 0),
+                                                         (128, "f32", 0, 0), (40, "f32", 3, 1)])
+def test_graph_capture_replays(fc, K, dtype, schedule, max_blocks):
     """A step whose pointer tables are already on the device, called on the
     stream it last ran on, enqueues kernel launches only, so it can be
     captured in a HIP graph.  Every replay (with eager steps and
     synchronizations in between) gives the bits of an eager twin plan."""
     import torch
     segs = table(13000 + K, dtype, nseg=4, max_len=3000)
+    if max_blocks:  # one block of 160 tile slots: the resident step takes several rounds (launches)
+        segs = segs + [(segs[-1][0] + segs[-1][1] + 64 - (segs[-1][0] + segs[-1][1]) % 64, 45000, 1.0, 1.0)]
     n = alloc_len(segs)
     rng = np.random.default_rng(K)
     npdt = np.float16 if dtype == "f16" else np.float32
@@ -383,8 +386,10 @@ def test_graph_capture_replays(fc, K, dtype, schedule):
     w0 = (rng.standard_normal(n, dtype=np.float32) * np.float32(0.05))
     wa, va = to_dev(w0), torch.zeros(n, device="cuda")
     wb, vb = to_dev(w0), torch.zeros(n, device="cuda")
-    pa = fc.Plan(segs, K, dtype, "tree", schedule=schedule)
-    pb = fc.Plan(segs, K, dtype, "tree", schedule=schedule)
+    pa = fc.Plan(segs, K, dtype, "tree", schedule=schedule, max_blocks=max_blocks)
+    pb = fc.Plan(segs, K, dtype, "tree", schedule=schedule, max_blocks=max_blocks)
+    if max_blocks:
+        assert pa.info().rounds >= 2
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
