@@ -151,13 +151,14 @@ typedef struct {
  * tables on the current device with hipMalloc (FC_EHIP on failure); when
  * fc_step's schedule resolves to TWO_PASS the plan also owns a raw-sum
  * scratch buffer of 4 bytes per element of the segment extent.
+ *   gdt   : an fc_dtype value, order: an fc_order value (plain ints, so that
+ *           any value a caller passes is defined; others are FC_EINVAL)
  * On success *plan receives the plan; on failure *plan is set to NULL. */
-int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,
-                   fc_order order);
+int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, int gdt, int order);
 
 /* As fc_plan_create, with an explicit launch shape (NULL = defaults). */
-int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt,
-                      fc_order order, const fc_launch_opts* opts);
+int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, int gdt, int order,
+                      const fc_launch_opts* opts);
 
 /* Free the plan and its device tables (NULL is ignored).  The caller must
  * make sure no work that uses the plan is still running. */

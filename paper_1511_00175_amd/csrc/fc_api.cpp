@@ -284,14 +284,16 @@ const char* fc_strerror(int code) {
     }
 }
 
-int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt, fc_order order,
+int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, int gdt_in, int order_in,
                       const fc_launch_opts* opts) {
     if (!plan) return FC_EINVAL;
     *plan = nullptr;
     if (nseg < 0 || (nseg > 0 && !segs)) return FC_EINVAL;
     if (K < 1 || K > K_MAX) return FC_EINVAL;
-    if (gdt != FC_F32 && gdt != FC_F16) return FC_EINVAL;
-    if (order != FC_ORDER_TREE && order != FC_ORDER_LINEAR) return FC_EINVAL;
+    if (gdt_in != FC_F32 && gdt_in != FC_F16) return FC_EINVAL;
+    if (order_in != FC_ORDER_TREE && order_in != FC_ORDER_LINEAR) return FC_EINVAL;
+    const fc_dtype gdt = static_cast<fc_dtype>(gdt_in);
+    const fc_order order = static_cast<fc_order>(order_in);
     const int vec = 4;
     uint64_t end = 0, n_elems = 0;
     for (int j = 0; j < nseg; ++j) {
@@ -454,7 +456,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, f
     return FC_OK;
 }
 
-int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, fc_dtype gdt, fc_order order) {
+int fc_plan_create(fc_plan** plan, const fc_segment* segs, int nseg, int K, int gdt, int order) {
     return fc_plan_create_ex(plan, segs, nseg, K, gdt, order, nullptr);
 }
 
