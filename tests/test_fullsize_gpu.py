@@ -90,3 +90,43 @@ def test_fullsize_fused_equals_composed(fc):
     assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
     assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
     plan.close()
+
+
+@pytest.mark.parametrize("dtype,schedule", [("f16", 1), ("f16", 3), ("f32", 2), ("f32", 3)])
+def test_offsets_beyond_4gib(fc, dtype, schedule):
+    """A segment of 2^31 + 100 elements: element indices pass 2^31 and byte
+    offsets pass 4 GiB (8 GiB of fp32) in every buffer, the tile map holds
+    8.4 M tiles and the resident schedule takes about 200 rounds.  Windows at
+    the start, around element 2^31 and at the end are recomputed by the oracle
+    from the gathered inputs (elements are independent within a segment)."""
+    import torch
+    dev = torch.device("cuda:0")
+    big = (1 << 31) + 100
+    rows = [(0, 1000, 1.0, 1.0), (1024, big, 2.0, 0.5)]
+    n = 1024 + big + 28
+    K = 2
+    g = torch.Generator(device=dev)
+    g.manual_seed(31)
+    tdt = torch.float16 if dtype == "f16" else torch.float32
+    reps = torch.empty((K, n), dtype=tdt, device=dev)
+    for k in range(K):
+        reps[k] = (torch.randn(n, generator=g, device=dev) * 1e-3).to(tdt)
+    w = torch.randn(n, generator=g, device=dev) * 0.01
+    v = torch.randn(n, generator=g, device=dev) * 1e-4
+    # windows inside one segment each: element 2^31 sits at byte 4 GiB of an
+    # fp16 replica and at byte 8 GiB of an fp32 replica, w and v
+    wins = [(0, 1000), (1024, 1024 + 512), ((1 << 31) - 256, (1 << 31) + 256), (1024 + big - 512, 1024 + big)]
+    before = [(reps[:, a:b].cpu().numpy(), w[a:b].cpu().numpy(), v[a:b].cpu().numpy()) for a, b in wins]
+    plan = fc.Plan(rows, K, dtype, "tree", schedule=schedule)
+    if schedule == 3:
+        assert plan.info().rounds > 100
+    plan.step(reps, w, v, 0.01, 0.9, 5e-4, 256)
+    torch.cuda.synchronize()
+    plan.close()
+    for (a, b), (r_h, w_h, v_h) in zip(wins, before):
+        seg = [r for r in rows if r[0] <= a < r[0] + r[1]][0]
+        ew, ev, _, _ = oracle.step([(0, b - a, seg[2], seg[3])], list(r_h), w_h, v_h, 0.01, 0.9, 5e-4, 256)
+        assert same_bits(w[a:b].cpu().numpy(), ew) == 0, (a, b)
+        assert same_bits(v[a:b].cpu().numpy(), ev) == 0, (a, b)
+    del reps, w, v
+    torch.cuda.empty_cache()
