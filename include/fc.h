@@ -101,8 +101,9 @@ typedef struct fc_plan fc_plan;
  *   LDS (1 KiB per 256-element tile: about 10 M parameters per round over 256
  *   compute units of 160 KiB); larger plans take several rounds, one launch
  *   per round.  It also
- *   makes fc_tree_reduce store the sums only after each read phase.  Uses the
- *   tile shape (1 vector, 16 replicas, 64 lanes) and no K split.
+ *   makes fc_tree_reduce store the sums only after each read phase.  Tiles of
+ *   64 lanes x 1 vector with batches of 16 replicas (default), or x 2 vectors
+ *   with batches of 4 (vecs_per_thread 2, K < 512); no K split.
  * AUTO (no launch-shape field given): RESIDENT when one round holds the plan
  *   or a parameter's replicas take at least 64 bytes (K * bytes per element),
  *   else FUSED.  With a launch-shape field: TWO_PASS when they take more than
@@ -117,7 +118,8 @@ typedef enum {
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero selects the default, which depends on the
  * schedule, the replica type, K and the plan's size (measured on MI355X):
- * RESIDENT -> (1 vector, 16 replicas, 64-lane tiles); otherwise fp32 in tree
+ * RESIDENT -> (1 vector, 16 replicas, 64-lane tiles), where vecs_per_thread
+ * and kchunk may also name (2, 4); otherwise fp32 in tree
  * order with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8
  * waves (see k_waves); fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
  * 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads

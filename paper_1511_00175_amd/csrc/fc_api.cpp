@@ -158,10 +158,15 @@ int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc_order order, int K, 
         // an explicit shape without k_waves asks for the unsplit kernel
         shape_given = o->block_threads || o->vecs_per_thread || o->kchunk || o->k_waves;
         if (o->schedule == FC_SCHED_RESIDENT) {
-            // the resident kernel has one shape: 64 lanes, 1 vector, batches of 16
-            if (o->k_waves > 1 || (o->block_threads && o->block_threads != 64) ||
-                (o->vecs_per_thread && o->vecs_per_thread != 1) || (o->kchunk && o->kchunk != 16))
+            // the resident kernel's tiles: 64 lanes of (1 vector, batches of 16)
+            // or (2 vectors, batches of 4); no K split.  The plan sets the shape.
+            const int ru = o->vecs_per_thread ? o->vecs_per_thread : 1;
+            const int rc = o->kchunk ? o->kchunk : (ru == 2 ? 4 : 16);
+            if (o->k_waves > 1 || (o->block_threads && o->block_threads != 64) || !fc::resident_pair(ru, rc) ||
+                !fc::resident_fits_k(ru, rc, K))
                 return FC_EINVAL;
+            sh.kwaves = 1;
+            return FC_OK;
         }
         if (o->k_waves) w = o->k_waves;
         else if (shape_given) w = 1;
@@ -319,10 +324,18 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
         hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess)
         return FC_EHIP;
+    int res_u = 1, res_c = 16;  // the resident tiles' lane vectors and batch
+    if (sched_req == FC_SCHED_RESIDENT && opts->vecs_per_thread) {
+        res_u = opts->vecs_per_thread;
+        res_c = opts->kchunk ? opts->kchunk : (res_u == 2 ? 4 : 16);
+    } else if (sched_req == FC_SCHED_RESIDENT && opts->kchunk) {
+        res_c = opts->kchunk;
+    }
+    const uint64_t tile_vecs_r = 64 * static_cast<uint64_t>(res_u);
     uint64_t res_tiles = 0;
     for (int j = 0; j < nseg; ++j)
-        res_tiles += (segs[j].length / vec + 63) / 64 + (segs[j].length % vec ? 1 : 0);
-    const uint64_t slot_bytes = fc::RESIDENT_SLOT * sizeof(float);
+        res_tiles += (segs[j].length / vec + tile_vecs_r - 1) / tile_vecs_r + (segs[j].length % vec ? 1 : 0);
+    const uint64_t slot_bytes = fc::RESIDENT_SLOT * sizeof(float) * res_u;
     const uint64_t cap = std::max<uint64_t>(1, static_cast<uint64_t>(std::max(lds_cu, 0)) / slot_bytes);
     int res_grid = std::max(1, cus);
     if (opts && opts->max_blocks > 0) res_grid = std::min(res_grid, opts->max_blocks);
@@ -337,8 +350,8 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
          fc::default_resident(K, gdt == FC_F16 ? 2 : 4, static_cast<int64_t>(res_rounds)));
     if (resident) {
         sh.block = 64;
-        sh.vecs = 1;
-        sh.kchunk = 16;
+        sh.vecs = res_u;
+        sh.kchunk = res_c;
         sh.kwaves = 1;
         sh.span = K;
         sh.lanes = 64;

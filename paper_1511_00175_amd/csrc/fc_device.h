@@ -565,11 +565,12 @@ __global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ?
 // so the whole grid streams one region of the parameters at a time.  Blocks
 // share nothing, so the result does not depend on how many of them are
 // resident at once.
-template <int DT, int W, int C, int MAXD, bool TREE, int MODE>
+template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE>
 __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
     extern __shared__ float slots[];
     const ReduceArgs& a = ra.r;
     constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
+    constexpr int SLOT = RESIDENT_SLOT * U;  // floats of LDS per tile of 64 * U vectors
     const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const uint32_t lane = threadIdx.x & 63;
     for (int round = 0; round < ra.rounds; ++round) {
@@ -578,15 +579,23 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
         const int hi = ldc(ra.ranges, b + 1);
         for (int t = lo + q; t < hi; t += W) {
             const Tile tile = ld_tile(a.tiles, t);
-            float* slot = slots + (t - lo) * RESIDENT_SLOT;
-            const uint32_t vi = lane < tile.count ? lane : 0u;  // idle lanes re-read the first vector
+            float* slot = slots + (t - lo) * SLOT;
             if (!(tile.seg & TAIL_BIT)) {
-                const uint32_t off[1] = {vi * 4 * SG};
-                Acc<1, 4> x;
-                reduce<DT, 4, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+                // vector u of the lane is tile vector lane + 64 u; idle lanes re-read vector 0
+                uint32_t off[U];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) slot[lane * 4 + i] = x.a[0][i];
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t vi = lane + 64 * u;
+                    off[u] = (vi < tile.count ? vi : 0u) * 4 * SG;
+                }
+                Acc<U, 4> x;
+                reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) slot[(lane + 64 * u) * 4 + i] = x.a[u][i];
             } else {
+                const uint32_t vi = lane < tile.count ? lane : 0u;
                 const uint32_t off[1] = {vi * SG};
                 Acc<1, 1> x;
                 reduce<DT, 1, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
@@ -598,17 +607,23 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
         for (int e = static_cast<int>(threadIdx.x); e < n; e += 64 * W) {
             const int j = __builtin_amdgcn_readfirstlane(e / 64);  // one tile per wave
             const Tile tile = ld_tile(a.tiles, lo + j);
-            if (lane >= tile.count) continue;
             float lr_j = 0.0f, wd_j = 0.0f;
             if constexpr (MODE == MODE_STEP) {
                 const int sj = static_cast<int>(tile.seg & SEG_MASK);
                 lr_j = a.lr * ldc(a.mults, 2 * sj);
                 wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
             }
-            const float* slot = slots + j * RESIDENT_SLOT;
+            const float* slot = slots + j * SLOT;
             const uint64_t start4 = tile.start * 4;
-            if (!(tile.seg & TAIL_BIT)) finish<4, MODE>(a, start4, lane * 16, slot + lane * 4, lr_j, wd_j);
-            else finish<1, MODE>(a, start4, lane * 4, slot + lane, lr_j, wd_j);
+            if (!(tile.seg & TAIL_BIT)) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t vi = lane + 64 * u;
+                    if (vi < tile.count) finish<4, MODE>(a, start4, vi * 16, slot + vi * 4, lr_j, wd_j);
+                }
+            } else if (lane < tile.count) {
+                finish<1, MODE>(a, start4, lane * 4, slot + lane, lr_j, wd_j);
+            }
         }
         __syncthreads();  // the next round's phase 1 overwrites the slots
     }
@@ -752,13 +767,22 @@ hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArg
 
 // The resident kernel instance for a plan's shape: f(kernel instance tag).
 template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F&& f) {
-    if (sh.vecs != 1 || sh.kchunk != 16 || sh.block != 64) return hipErrorInvalidValue;
-    return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
-        return pick_maxd(sh.maxd, [&](auto d) {
-            if (sh.tree) return f(&resident_kernel<DT, RESIDENT_WAVES, 16, d.value, true, md.value>);
-            return f(&resident_kernel<DT, RESIDENT_WAVES, 16, d.value, false, md.value>);
+    if (sh.block != 64) return hipErrorInvalidValue;
+    auto go = [&](auto u, auto c) {
+        return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
+            auto at = [&](auto d) {
+                if (sh.tree) return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, true, md.value>);
+                return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, false, md.value>);
+            };
+            if constexpr (u.value == 1) return pick_maxd(sh.maxd, at);
+            else return sh.maxd <= 5 ? at(I<5>{}) : at(I<7>{});
         });
-    });
+    };
+    // (lane vectors, replicas per batch) of the resident tiles; two vectors
+    // per lane only with stacks up to depth 7 (deeper ones would spill)
+    if (sh.vecs == 1 && sh.kchunk == 16) return go(I<1>{}, I<16>{});
+    if (sh.vecs == 2 && sh.kchunk == 4 && sh.maxd <= 7) return go(I<2>{}, I<4>{});
+    return hipErrorInvalidValue;
 }
 
 // Allow `lds` bytes of dynamic LDS for the plan's resident kernels (both

@@ -62,7 +62,7 @@ struct ResidentArgs {
     const int* ranges;            // gridDim.x * rounds + 1 tile indices
     int rounds;
 };
-constexpr int RESIDENT_SLOT = 256;
+constexpr int RESIDENT_SLOT = 256;  // floats per tile of 64 lanes x one 4-element vector
 constexpr int RESIDENT_WAVES = 16;
 
 struct SgdArgs {

@@ -55,6 +55,11 @@ inline int ksplit_span(int K, int w, int c) {
     return s;
 }
 
+// (lane vectors, replicas per batch) of the resident kernel's tiles; with
+// two vectors per lane K / kchunk must stay below 128 (stack depth 7).
+inline bool resident_pair(int u, int c) { return (u == 1 && c == 16) || (u == 2 && c == 4); }
+inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128; }
+
 inline bool compiled_pair(int u, int c) {
     return (u == 1 && (c == 8 || c == 16)) || (u == 2 && (c == 8 || c == 16)) ||
            (u == 4 && (c == 2 || c == 4 || c == 8));

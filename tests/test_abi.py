@@ -63,6 +63,8 @@ def test_strerror(fcmod):
     ([(0, 16)], 4, 0, {"schedule": 3, "vecs_per_thread": 4}, -1),
     ([(0, 16)], 4, 0, {"schedule": 3, "block_threads": 128}, -1),
     ([(0, 16)], 4, 0, {"schedule": 3, "kchunk": 8}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 3, "vecs_per_thread": 2, "kchunk": 8}, -1),
+    ([(0, 16)], 512, 0, {"schedule": 3, "vecs_per_thread": 2}, -1),   # two vectors: K / 4 < 128
 ])
 def test_plan_argument_errors(fcmod, segs, K, gdt, opts, code):
     rc, h = fcmod._fc.fc_plan_create(segs, K, gdt, 0, opts)

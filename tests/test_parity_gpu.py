@@ -426,14 +426,16 @@ def test_read_probe_reads_every_byte(fc):
 
 @pytest.mark.parametrize("order", ["tree", "linear"])
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("K,max_blocks", [(1, 0), (17, 0), (100, 3), (1024, 0), (33, 1)])
-def test_resident_matches_oracle(fc, K, max_blocks, dtype, order):
+@pytest.mark.parametrize("K,max_blocks,vecs", [(1, 0, 1), (17, 0, 1), (100, 3, 1), (1024, 0, 1), (33, 1, 1),
+                                               (1, 0, 2), (30, 2, 2), (128, 0, 2), (511, 1, 2)])
+def test_resident_matches_oracle(fc, K, max_blocks, vecs, dtype, order):
     """The resident schedule (phase 1: reduce each block's tiles into LDS;
-    phase 2: finish them from LDS): reduce and steps with raw sum and
-    broadcast, blocks with one tile or with many, both orders."""
-    segs = table(14000 + K, dtype, nseg=5, max_len=3000 if K < 1000 else 800)
+    phase 2: finish them from LDS), with tiles of 64 lanes x 1 vector
+    (batches of 16) or x 2 vectors (batches of 4): reduce and steps with raw
+    sum and broadcast, blocks with one tile or with many, both orders."""
+    segs = table(14000 + K, dtype, nseg=5, max_len=3000 if K < 500 else 800)
     rng = np.random.default_rng(K + 3)
-    opts = dict(schedule=3, max_blocks=max_blocks)
+    opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     bad, _, _ = run_reduce(fc, segs, K, dtype, order, rng, opts=opts)
     assert bad == 0
     assert run_steps(fc, segs, K, dtype, order, rng, steps=2, opts=opts, with_out=True,
@@ -441,18 +443,18 @@ def test_resident_matches_oracle(fc, K, max_blocks, dtype, order):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("K,max_blocks", [(5, 1), (33, 2), (130, 1)])
-def test_resident_rounds_match_oracle(fc, K, max_blocks, dtype):
+@pytest.mark.parametrize("K,max_blocks,vecs", [(5, 1, 1), (33, 2, 1), (130, 1, 1), (40, 1, 2)])
+def test_resident_rounds_match_oracle(fc, K, max_blocks, vecs, dtype):
     """A plan larger than the grid's LDS takes several rounds (here with 1-3
     blocks of 160 tile slots each); every round's ranges are finished before
     the next round's reduce reuses the slots."""
     rows = [(0, 50000, 1, 1), (50048, 7, 2.0, 0.0), (50112, 60001, 1, 1)]
-    p = fc.Plan(rows, K, dtype, "tree", schedule=3, max_blocks=max_blocks)
+    p = fc.Plan(rows, K, dtype, "tree", schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     info = p.info()
     p.close()
-    assert info.rounds >= 2 and info.grid == max_blocks
+    assert info.rounds >= 2 and info.grid == max_blocks and info.vecs_per_thread == vecs
     rng = np.random.default_rng(K)
-    opts = dict(schedule=3, max_blocks=max_blocks)
+    opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     bad, _, _ = run_reduce(fc, rows, K, dtype, "tree", rng, opts=opts)
     assert bad == 0
     assert run_steps(fc, rows, K, dtype, "tree", rng, steps=2, opts=opts, with_out=True) == 0
