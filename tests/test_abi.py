@@ -144,3 +144,13 @@ def test_read_probe_argument_errors(fcmod):
     assert f.fc_read_probe(72, 16, 64, None) == f.FC_EALIGN     # source not 16-byte aligned
     assert f.fc_read_probe_blocks(1) == 1 and f.fc_read_probe_blocks(16384) == 1
     assert f.fc_read_probe_blocks(16384 + 16) == 2
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/fc.h is a C header: strict C99 with every warning an error."""
+    import subprocess
+    src = tmp_path / "use_fc.c"
+    src.write_text('#include "fc.h"\nint main(void) { return fc_strerror(FC_OK) == 0; }\n')
+    r = subprocess.run(["gcc", "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-fsyntax-only",
+                        f"-I{os.path.join(ROOT, 'include')}", str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
