@@ -43,13 +43,23 @@ KERNEL_SOURCES = ("fc_device.h", "fc_internal.h", "fc_shape.h", "fc_reduce_f32.h
                   "fc_update.hip")
 
 
+def _code_tokens(text):
+    """C++ source with comments removed and whitespace collapsed (the sources
+    hashed here hold no string literal with comment markers)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_hash():
     """Hash of what decides the kernels that run: the device code and the
-    launch-shape / schedule rules (host-only code is left out)."""
+    launch-shape / schedule rules (host-only code is left out), comments and
+    layout ignored."""
     h = hashlib.sha256()
     for fn in KERNEL_SOURCES:
-        with open(os.path.join(CSRC, fn), "rb") as f:
-            h.update(fn.encode() + b"\0" + f.read())
+        with open(os.path.join(CSRC, fn), encoding="utf-8") as f:
+            h.update(fn.encode() + b"\0" + _code_tokens(f.read()).encode())
     return h.hexdigest()[:16]
 
 

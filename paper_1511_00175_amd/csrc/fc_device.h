@@ -27,6 +27,16 @@
 //   ga = s*c ; d = ga + wd_j*w ; v' = mu*v + lr_j*d ; w' = w - v'
 // Every operation is one rounded fp32 op: contraction is disabled below and
 // the library is built with -ffp-contract=off.
+//
+// Kernels (all share the loads, the register stack and the epilogue, so they
+// give the same bits):
+//   reduce_kernel   one tile per block; reduce-only, or the fused step
+//   ksplit_kernel   the K replicas split over the waves of a block, combined
+//                   in tree order through LDS
+//   resident_kernel one persistent block per CU: reduce a range of tiles into
+//                   LDS (pure reads), then finish it from LDS
+//   sgd_kernel      the update from a raw sum (second pass of two)
+//   bcast_kernel    copy one vector into K destinations
 #pragma once
 
 #include <type_traits>
