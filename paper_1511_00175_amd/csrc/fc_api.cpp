@@ -451,7 +451,9 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         ok = hipMalloc(reinterpret_cast<void**>(&p->d_ranges), ranges.size() * sizeof(int)) == hipSuccess &&
              hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) == hipSuccess;
         if (ok) {
-            const size_t lds = static_cast<size_t>(p->res_lds);
+            // the attribute belongs to the kernel, not to the plan: allow the
+            // compute unit's whole LDS, so that no plan lowers another's limit
+            const size_t lds = static_cast<size_t>(lds_cu);
             ok = (gdt == FC_F16 ? fc::prepare_resident_f16(sh, lds) : fc::prepare_resident_f32(sh, lds)) ==
                  hipSuccess;
         }

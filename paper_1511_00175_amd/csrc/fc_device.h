@@ -795,8 +795,9 @@ template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F
     return hipErrorInvalidValue;
 }
 
-// Allow `lds` bytes of dynamic LDS for the plan's resident kernels (both
-// modes), on the current device; called once when a plan is created.
+// Allow up to `lds` bytes of dynamic LDS for the plan's resident kernels
+// (both modes) on the current device; called when a plan is created.  The
+// limit is a property of the kernel, shared by every plan that uses it.
 template <int DT>
 hipError_t prepare_resident_dt(const Shape& sh, size_t lds) {
     for (int mode : {static_cast<int>(MODE_REDUCE), static_cast<int>(MODE_STEP)}) {

@@ -458,3 +458,30 @@ def test_resident_rounds_match_oracle(fc, K, max_blocks, vecs, dtype):
     bad, _, _ = run_reduce(fc, rows, K, dtype, "tree", rng, opts=opts)
     assert bad == 0
     assert run_steps(fc, rows, K, dtype, "tree", rng, steps=2, opts=opts, with_out=True) == 0
+
+
+def test_resident_plans_with_different_lds_interleave(fc):
+    """Plans whose resident blocks need different amounts of LDS share the
+    same kernel: creating a small plan after a large one must not break the
+    large one's launches."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    big_n = cus * 150 * 256  # 150 tiles per block
+    K = 4
+    rows_big = [(0, big_n, 1.0, 1.0)]
+    rows_small = [(0, 3000, 1.0, 1.0)]
+    rng = np.random.default_rng(77)
+    big = fc.Plan(rows_big, K, "f32", "tree", schedule=3)
+    small = fc.Plan(rows_small, K, "f32", "tree", schedule=3)
+    assert big.info().lds_bytes == 150 * 1024 and small.info().lds_bytes == 1024
+    reps = torch.from_numpy(rng.standard_normal((K, big_n), dtype=np.float32)).cuda()
+    out = torch.full((big_n,), -1.0, device="cuda")
+    big.tree_reduce(reps, out)
+    small.tree_reduce(reps, out)
+    big.tree_reduce(reps, out)
+    torch.cuda.synchronize()
+    x = reps.cpu().numpy()
+    expect = (x[0] + x[1]) + (x[2] + x[3])
+    assert same_bits(out.cpu().numpy(), expect) == 0
+    big.close()
+    small.close()
