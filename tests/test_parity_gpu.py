@@ -485,3 +485,15 @@ def test_resident_plans_with_different_lds_interleave(fc):
     assert same_bits(out.cpu().numpy(), expect) == 0
     big.close()
     small.close()
+
+
+@pytest.mark.parametrize("batch", [1, 3, 1000, 65535])
+def test_batch_not_a_power_of_two(fc, batch):
+    """c = fl(1/batch) is inexact for most batches, so ga = s * c rounds: both
+    sides compute c once on the host in fp32 and must agree bit for bit, in
+    every schedule."""
+    segs = table(15000 + batch, "f32", nseg=4, max_len=2500)
+    for schedule in (1, 2, 3):
+        rng = np.random.default_rng(batch + schedule)
+        assert run_steps(fc, segs, 20, "f32", "tree", rng, steps=2, opts=dict(schedule=schedule),
+                         batch=batch) == 0, schedule
