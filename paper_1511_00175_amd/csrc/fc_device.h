@@ -548,7 +548,7 @@ __device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, ui
 template <int DT, int W, int U, int C, int D, int MODE>
 __global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ? 8 : 1) void ksplit_kernel(
     ReduceArgs a) {
-    __shared__ float part[W * U * 64 * 4];
+    __shared__ __attribute__((aligned(16))) float part[W * U * 64 * 4];
     for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
         const Tile tile = ld_tile(a.tiles, t);
         float lr_j = 0.0f, wd_j = 0.0f;
@@ -577,7 +577,9 @@ __global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ?
 // resident at once.
 template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE>
 __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
-    extern __shared__ float slots[];
+    // 16-byte aligned, so that a lane's 4 sums move as one 16-byte LDS access
+    extern __shared__ f4 slot_vecs[];
+    float* slots = reinterpret_cast<float*>(slot_vecs);
     const ReduceArgs& a = ra.r;
     constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
     constexpr int SLOT = RESIDENT_SLOT * U;  // floats of LDS per tile of 64 * U vectors
