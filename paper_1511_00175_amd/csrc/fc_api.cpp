@@ -73,21 +73,21 @@ struct Span {
     bool replica;
 };
 
-bool overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
-
 // Written buffers may not overlap any other buffer, except that `out` may be
 // exactly a replica of an FC_F32 plan (each element is read by the thread
-// that writes it).  Read-only buffers may overlap each other.
-int check_aliasing(const std::vector<Span>& spans, int out_id, bool f32) {
+// that writes it).  Read-only buffers may overlap each other.  The spans are
+// sorted by start and each is compared only with the spans that start
+// before it ends, so a valid call costs O(n log n) for n = K + a few spans.
+int check_aliasing(std::vector<Span>& spans, int out_id, bool f32) {
+    spans.erase(std::remove_if(spans.begin(), spans.end(), [](const Span& x) { return x.hi == x.lo; }),
+                spans.end());
+    std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.lo < y.lo; });
     const size_t n = spans.size();
     for (size_t i = 0; i < n; ++i) {
         const Span& a = spans[i];
-        if (a.hi == a.lo) continue;
-        for (size_t j = i + 1; j < n; ++j) {
-            const Span& b = spans[j];
-            if (b.hi == b.lo) continue;
+        for (size_t j = i + 1; j < n && spans[j].lo < a.hi; ++j) {
+            const Span& b = spans[j];  // overlaps a: b.lo >= a.lo and b.lo < a.hi
             if (!a.written && !b.written) continue;
-            if (!overlap(a, b)) continue;
             const bool exact_out_alias =
                 f32 && ((a.id == out_id && b.replica) || (b.id == out_id && a.replica)) && a.lo == b.lo &&
                 a.hi == b.hi;

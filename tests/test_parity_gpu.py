@@ -348,9 +348,16 @@ def test_argument_errors_need_a_plan(fc):
     # a broadcast destination overlapping w
     assert f.fc_step(h, reps, w.data_ptr(), v.data_ptr(), 0.1, 0.9, 0.0, 1, None, dst[:3] + [w.data_ptr()],
                      s) == f.FC_EALIAS
+    # w inside a replica; v ending inside w; the raw sum exactly on w
+    assert f.fc_step(h, reps, reps[2] + 64, v.data_ptr(), 0.1, 0.9, 0.0, 1, None, None, s) == f.FC_EALIAS
+    assert f.fc_step(h, reps, w.data_ptr(), w.data_ptr() - 16, 0.1, 0.9, 0.0, 1, None, None, s) == f.FC_EALIAS
+    assert f.fc_step(h, reps, w.data_ptr(), v.data_ptr(), 0.1, 0.9, 0.0, 1, w.data_ptr(), None, s) == f.FC_EALIAS
     torch.cuda.synchronize()
     # nothing was written by the rejected calls
     assert float(out.abs().sum()) == 0.0 and float(w.abs().sum()) == 0.0
+    # read-only buffers may overlap: every replica the same pointer is a valid call
+    assert f.fc_tree_reduce(h, [reps[0]] * 4, out.data_ptr(), s) == f.FC_OK
+    torch.cuda.synchronize()
 
 
 def test_empty_and_zero_length(fc):
