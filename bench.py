@@ -529,6 +529,14 @@ def main():
     if probes:
         res["config"]["probes"] = probes
         res["roofline"]["frac_of_read_probe"] = round(achieved / probes["read_gbs"], 4)
+        # a ceiling from the two probes: the replicas at the streaming-read rate,
+        # then w, v read and written at the copy rate (the path's bytes, each at
+        # the best rate this GPU showed for that kind of traffic)
+        rep = wl.n_params * wl.K * wl.s_g
+        rest = bytes_step - rep
+        model_us = (rep / probes["read_gbs"] + rest / probes["copy_gbs"]) / 1e3
+        res["roofline"]["probe_model"] = {"us_per_step": round(model_us, 2),
+                                          "frac": round(model_us / (ms_per_step * 1e3), 4)}
     if graph:
         res["graph"] = graph
     if not args.no_cpu_baseline:
