@@ -504,3 +504,28 @@ def test_batch_not_a_power_of_two(fc, batch):
         rng = np.random.default_rng(batch + schedule)
         assert run_steps(fc, segs, 20, "f32", "tree", rng, steps=2, opts=dict(schedule=schedule),
                          batch=batch) == 0, schedule
+
+
+@pytest.mark.parametrize("n,K,max_blocks,vecs", [(1000, 4, 0, 1), (5_000_000, 8, 0, 1), (40_000_000, 8, 0, 1),
+                                                 (143_667_240, 16, 0, 1), (60_965_224, 128, 0, 2),
+                                                 (300_000, 8, 3, 1), (1, 1, 0, 1)])
+def test_resident_partition(fc, n, K, max_blocks, vecs):
+    """The resident plan's grid, rounds and LDS per block follow from the tile
+    count and the CU's LDS: rounds = ceil(tiles / (grid * slots)), each of the
+    grid * rounds ranges holds at most ceil(tiles / (grid * rounds)) tiles of
+    64 * vecs vectors, each with 1 KiB * vecs of LDS (160 KiB per CU)."""
+    import math
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    p = fc.Plan([(0, n, 1, 1)], K, "f32", "tree", schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    info = p.info()
+    p.close()
+    tiles = (n // 4 + 64 * vecs - 1) // (64 * vecs) + (1 if n % 4 else 0)
+    grid = min(cus, max_blocks) if max_blocks else cus
+    grid = min(grid, tiles)
+    slots = (160 * 1024) // (1024 * vecs)
+    rounds = max(1, math.ceil(tiles / (grid * slots)))
+    per = math.ceil(tiles / (grid * rounds))
+    assert (info.ntiles, info.grid, info.rounds, info.lds_bytes) == (tiles, grid, rounds, per * 1024 * vecs), \
+        (info.ntiles, info.grid, info.rounds, info.lds_bytes)
+    assert info.lds_bytes <= 160 * 1024
