@@ -162,6 +162,19 @@ def pin_tree_structure():
             assert _same(got, _balanced(x)), K
 
 
+def pin_tree_shards():
+    """Sharding over workers keeps the tree's bits (Sec. 6.2 tree over p
+    nodes): cut the K leaves into aligned runs of S = 2^m (the last one
+    shorter), reduce each run, then reduce the run sums in order -- the result
+    is the tree over all K leaves.  This is what lets G GPUs each reduce their
+    own workers' subtree and one owner combine the G partials."""
+    rng = np.random.default_rng(6)
+    for K, S in ((128, 16), (128, 1), (128, 128), (100, 16), (37, 8), (1000, 64), (7, 4), (130, 32)):
+        x = (rng.standard_normal((K, 48)) * np.exp(rng.standard_normal((K, 1)) * 3)).astype(np.float32)
+        parts = np.stack([_reduce(x[i:i + S], "tree") for i in range(0, K, S)])
+        assert _same(_reduce(parts, "tree"), _reduce(x, "tree")), (K, S)
+
+
 def pin_linear_structure():
     """Parameter-server order: the running sum x0+x1, then +x2, ... (numpy
     cumulative sum in float32 adds left to right)."""
@@ -340,6 +353,6 @@ def pin_lr_poly_closed_forms():
 
 
 PINS = [pin_f16_widen_exhaustive, pin_k1_identity, pin_all_ones, pin_integer_exact, pin_fsum_bound,
-        pin_order_golden, pin_tree_structure, pin_linear_structure, pin_ieee_special_sums,
+        pin_order_golden, pin_tree_structure, pin_tree_shards, pin_linear_structure, pin_ieee_special_sums,
         pin_ragged_segments_and_padding, pin_sgd_golden, pin_sgd_fp64_bound, pin_sgd_closed_forms,
         pin_broadcast, pin_step_composition, pin_lr_paper_values, pin_lr_poly_closed_forms]

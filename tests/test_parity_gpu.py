@@ -529,3 +529,32 @@ def test_resident_partition(fc, n, K, max_blocks, vecs):
     assert (info.ntiles, info.grid, info.rounds, info.lds_bytes) == (tiles, grid, rounds, per * 1024 * vecs), \
         (info.ntiles, info.grid, info.rounds, info.lds_bytes)
     assert info.lds_bytes <= 160 * 1024
+
+
+@pytest.mark.parametrize("K,S", [(128, 16), (100, 16), (1024, 128), (37, 8)])
+def test_sharded_reduction_equals_full_tree(fc, K, S):
+    """The multi-GPU plan on one GPU: each of the runs of S aligned workers
+    (one GPU's share) is reduced on its own, then the run sums are reduced in
+    order by a plan over ceil(K / S) inputs -- the same bits as one plan over
+    all K (the sharded allreduce design keeps parity)."""
+    import torch
+    n = 20000
+    rng = np.random.default_rng(K + S)
+    x = to_dev(rng.standard_normal((K, n), dtype=np.float32))
+    rows = [(0, n, 1, 1)]
+    full = torch.empty(n, device="cuda")
+    p = fc.Plan(rows, K, "f32", "tree")
+    p.tree_reduce(x, full)
+    p.close()
+    runs = [(i, min(S, K - i)) for i in range(0, K, S)]
+    parts = torch.empty((len(runs), n), device="cuda")
+    for r, (i, m) in enumerate(runs):
+        q = fc.Plan(rows, m, "f32", "tree")
+        q.tree_reduce([x[i + j] for j in range(m)], parts[r])
+        q.close()
+    top = torch.empty(n, device="cuda")
+    q = fc.Plan(rows, len(runs), "f32", "tree")
+    q.tree_reduce(parts, top)
+    q.close()
+    torch.cuda.synchronize()
+    assert same_bits(top.cpu().numpy(), full.cpu().numpy()) == 0
