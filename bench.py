@@ -357,6 +357,8 @@ def main():
                          "graph-amortized time per step")
     ap.add_argument("--no-probes", action="store_true",
                     help="skip the read and copy bandwidth probes reported beside the roofline")
+    ap.add_argument("--no-balance", action="store_true",
+                    help="keep equal resident shares (no fc_plan_balance after the warm-up)")
     ap.add_argument("--rotate", type=int, default=DEFAULT_ROTATE,
                     help="R independent input sets (replicas, w, v), step i using set i mod R, so that no "
                          "step finds the previous step's w and v in a cache (1: one set)")
@@ -414,6 +416,17 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # XCD-aware shares (resident schedule): each plan re-divides its tiles by
+    # the per-XCD rates of its launches so far, twice, with warm-up steps
+    # after each
+    balance = None
+    if not args.no_balance and info.schedule == 3:
+        for _ in range(2):
+            rates = [p.balance() for p in plans]
+            for _ in range(max(args.warmup, 2 * len(plans))):
+                step()
+            torch.cuda.synchronize()
+        balance = {"xcd_rate": [round(r, 4) for r in rates[0] if r > 0], "calls": 2}
     # timed region 1: the steps alone (barrier = device synchronize on both sides)
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -477,7 +490,8 @@ def main():
     dom = max(kernels, key=lambda k: kernels[k]["launches"] * kernels[k]["avg_us"])
     avg = kernels[dom]["avg_us"] * 1e-6
     achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
-    plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE)
+    plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE or
+                 args.no_balance)
     traffic = read_traffic(wl.name, dom) if plain else None
     sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
     rk = "ksplit_kernel" if info.k_waves > 1 else "resident_kernel" if info.schedule == 3 else "reduce_kernel"
@@ -507,6 +521,7 @@ def main():
                        "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "k_waves": info.k_waves,
                        "schedule": sched, "rounds": info.rounds, "lds_bytes": info.lds_bytes},
             "input_sets": args.rotate,
+            "balance": balance,
             "input_hash": input_hash(sets),
             "step_times": step_times,
             "kernels": kernels,

@@ -294,6 +294,30 @@ typedef struct {
 int fc_plan_set_timing(fc_plan* plan, int enable);
 int fc_plan_read_timing(fc_plan* plan, fc_timing* timing);
 
+/* XCD-aware shares for the RESIDENT schedule.  An MI355X runs the persistent
+ * grid's blocks on 8 XCDs (block b on XCD b mod 8), and blocks on some XCDs
+ * read HBM 6-10% more slowly than on others; every launch ends with its
+ * slowest block.  Each resident launch adds, per block, the tiles it reduced
+ * and the time its reduce phase took to a record the plan keeps, with the
+ * XCD the block ran on (hardware register XCC_ID).  This call waits for
+ * `stream` (a hipStream_t, NULL = the null stream: the stream of the plan's
+ * calls), reads the record of every launch since the plan was made or last
+ * balanced, clears it, and re-divides every round's tiles so that each
+ * block's share is proportional to the tiles per second measured on its XCD,
+ * drawn toward equal shares as far as needed for every share to fit a
+ * block's LDS.  Only which block
+ * reduces a tile changes: results are bit-identical before and after.  The
+ * new shares apply to every later launch, including launches of graphs
+ * captured before (the plan's device tables change in place; their sizes
+ * and the launches' LDS do not).  It must not overlap any call of the same
+ * plan on another stream.
+ * xcd_rate (nullable): n_rate floats, entry x = XCD x's measured rate relative
+ * to the mean over all blocks, 0 for an XCD that ran no block (at most 16 XCDs
+ * are reported).  A plan that is not RESIDENT, or has not launched since it
+ * was made or last balanced, is left as it is (FC_OK, rates 0).  Errors: FC_EINVAL (NULL plan,
+ * n_rate < 0, or n_rate > 0 with xcd_rate NULL), FC_EHIP, FC_ENOMEM. */
+int fc_plan_balance(fc_plan* plan, void* stream, float* xcd_rate, int n_rate);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,11 +11,11 @@ only marshals torch tensors (device memory and the current stream) into it.
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
                   FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
-                  fc_lr_at, fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks,
+                  fc_lr_at, fc_plan_balance, fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks,
                   fc_sgd_step, fc_step, fc_strerror, fc_train, fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
-           "fc_plan_read_timing", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
+           "fc_plan_read_timing", "fc_plan_balance", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
            "fc_lr_at", "fc_train", "lr_policy", "lr_at", "fc_read_probe", "fc_read_probe_blocks", "read_probe"]
 
 
@@ -105,6 +105,15 @@ class Plan:
     def read_timing(self):
         """{kernel: (launches, total us)} since the previous read."""
         return fc_plan_read_timing(self.handle)
+
+    def balance(self, stream=None):
+        """Re-divide the resident schedule's tiles by the per-XCD rates of the
+        last launch (fc_plan_balance); returns the rates (relative to the
+        mean, 0 for XCDs that ran no block)."""
+        rc, rates = fc_plan_balance(self.handle, _stream(stream))
+        if rc:
+            raise FcError("fc_plan_balance", rc)
+        return rates
 
     def tree_reduce(self, grads, out, stream=None):
         rc = fc_tree_reduce(self.handle, _rows(grads), _ptr(out), _stream(stream))

@@ -84,9 +84,10 @@ lib.fc_read_probe_blocks.restype = ctypes.c_uint64
 lib.fc_read_probe.argtypes = [_vp, ctypes.c_uint64, _vp, _vp]
 lib.fc_plan_set_timing.argtypes = [_plan_p, _i]
 lib.fc_plan_read_timing.argtypes = [_plan_p, ctypes.POINTER(fc_timing)]
+lib.fc_plan_balance.argtypes = [_plan_p, _vp, ctypes.POINTER(ctypes.c_float), _i]
 for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
            "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing", "fc_lr_at", "fc_train",
-           "fc_read_probe"):
+           "fc_read_probe", "fc_plan_balance"):
     getattr(lib, _n).restype = ctypes.c_int
 
 
@@ -156,6 +157,16 @@ def fc_plan_read_timing(plan):
     t = fc_timing()
     _check("fc_plan_read_timing", lib.fc_plan_read_timing(plan, ctypes.byref(t)))
     return {KERNEL_NAMES[i]: (t.launches[i], t.total_us[i]) for i in range(FC_KERNEL_KINDS)}
+
+
+N_XCD_RATES = 16
+
+
+def fc_plan_balance(plan, stream=0):
+    """Returns (rc, [relative rate of XCD x for x < 16], 0 where no block ran)."""
+    rates = (ctypes.c_float * N_XCD_RATES)()
+    rc = lib.fc_plan_balance(plan, stream, rates, N_XCD_RATES)
+    return rc, list(rates)
 
 
 def fc_tree_reduce(plan, grads, out, stream=0):

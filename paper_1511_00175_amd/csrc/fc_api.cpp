@@ -41,6 +41,10 @@ struct fc_plan {
     int res_grid = 0;
     int res_rounds = 0;
     int res_lds = 0;                 // RESIDENT: LDS bytes per block
+    int res_slot = 0;                // RESIDENT: LDS bytes per tile
+    std::vector<int> res_ranges;     // RESIDENT: host copy of the d_ranges table
+    unsigned long long* d_clock = nullptr;  // RESIDENT: per block, the kernel's phase-1 clock and XCD
+
 
     // per-kernel timing (fc_plan_set_timing / fc_plan_read_timing)
     struct Rec {
@@ -126,10 +130,11 @@ hipError_t launch_reduce(const fc::Shape& sh, int mode, int grid, const fc::Redu
 // one round's update writes never meet the next round's replica reads
 // (measured on MI355X, VGG-19 K=16 in 14 rounds: 1881 us vs 2076 us with
 // all rounds in one launch).
-hipError_t launch_resident(const fc_plan* p, int mode, const fc::ReduceArgs& r, hipStream_t s) {
+hipError_t launch_resident(fc_plan* p, int mode, const fc::ReduceArgs& r, hipStream_t s) {
     fc::ResidentArgs a{};
     a.r = r;
     a.rounds = 1;
+    a.clock = p->d_clock;
     const size_t lds = static_cast<size_t>(p->res_lds);
     for (int round = 0; round < p->res_rounds; ++round) {
         a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
@@ -139,6 +144,39 @@ hipError_t launch_resident(const fc_plan* p, int mode, const fc::ReduceArgs& r, 
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// Zero the per-block record of the resident launches (synchronous).
+hipError_t clear_clock(fc_plan* p) {
+    std::vector<unsigned long long> z(static_cast<size_t>(p->res_grid) * fc::RESIDENT_CLOCK_WORDS, 0ull);
+    return hipMemcpy(p->d_clock, z.data(), z.size() * sizeof(unsigned long long), hipMemcpyHostToDevice);
+}
+
+// The resident ranges for per-block weights w (one per block of the grid):
+// in every round, block b's share of the round's tiles is proportional to
+// w[b].  Returns the most tiles any block gets.
+int resident_ranges(int ntiles, int rounds, int grid, const std::vector<double>& w, std::vector<int>& ranges) {
+    std::vector<double> cum(static_cast<size_t>(grid) + 1, 0.0);
+    for (int b = 0; b < grid; ++b) cum[b + 1] = cum[b] + w[b];
+    ranges.assign(static_cast<size_t>(grid) * rounds + 1, 0);
+    int most = 0;
+    for (int r = 0; r < rounds; ++r) {
+        const uint64_t lo = static_cast<uint64_t>(ntiles) * r / rounds;
+        const uint64_t hi = static_cast<uint64_t>(ntiles) * (r + 1) / rounds;
+        ranges[static_cast<size_t>(r) * grid] = static_cast<int>(lo);
+        for (int b = 1; b < grid; ++b) {
+            uint64_t x = lo + static_cast<uint64_t>(static_cast<double>(hi - lo) * (cum[b] / cum[grid]));
+            x = std::min(hi, std::max<uint64_t>(x, ranges[static_cast<size_t>(r) * grid + b - 1]));
+            ranges[static_cast<size_t>(r) * grid + b] = static_cast<int>(x);
+        }
+        const int end = static_cast<int>(hi);
+        ranges[static_cast<size_t>(r + 1) * grid] = end;  // the next round's first, or the end
+        for (int b = 0; b < grid; ++b) {
+            const size_t i = static_cast<size_t>(r) * grid + b;
+            most = std::max(most, (b + 1 < grid ? ranges[i + 1] : end) - ranges[i]);
+        }
+    }
+    return most;
 }
 
 void note_stream(fc_plan* p, hipStream_t s) {
@@ -224,6 +262,7 @@ void free_plan(fc_plan* p) {
     for (auto e : p->event_pool) (void)hipEventDestroy(e);
     if (p->d_sum) (void)hipFree(p->d_sum);
     if (p->d_ranges) (void)hipFree(p->d_ranges);
+    if (p->d_clock) (void)hipFree(p->d_clock);
     if (p->d_tiles) (void)hipFree(p->d_tiles);
     if (p->d_mults) (void)hipFree(p->d_mults);
     if (p->d_grads) (void)hipFree(p->d_grads);
@@ -342,7 +381,12 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     if (res_tiles > 0 && res_tiles < static_cast<uint64_t>(res_grid)) res_grid = static_cast<int>(res_tiles);
     const uint64_t res_rounds = std::max<uint64_t>(1, (res_tiles + res_grid * cap - 1) / (res_grid * cap));
     const uint64_t res_ranges = static_cast<uint64_t>(res_grid) * res_rounds;
-    const uint64_t res_lds = (res_tiles + res_ranges - 1) / res_ranges * slot_bytes;
+    // LDS for the most tiles a block may ever hold, so that rebalanced
+    // ranges (fc_plan_balance) never need more than a launch already has,
+    // also in a captured graph (measured on MI355X: the size itself does
+    // not change the speed)
+    const uint64_t res_lds =
+        std::min<uint64_t>(cap, std::max<uint64_t>(1, (res_tiles + res_rounds - 1) / res_rounds)) * slot_bytes;
     if (res_ranges > static_cast<uint64_t>(INT32_MAX) - 1) return FC_EINVAL;
     const bool resident =
         sched_req == FC_SCHED_RESIDENT ||
@@ -425,11 +469,12 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     if (resident) p->schedule = FC_SCHED_RESIDENT;
     else p->schedule = sched_req == FC_SCHED_AUTO ? fc::default_schedule(K, p->sg) : sched_req;
     p->device = device;
-    std::vector<int> ranges;
+    std::vector<int>& ranges = p->res_ranges;
     if (resident) {
         p->res_grid = res_grid;
         p->res_rounds = static_cast<int>(res_rounds);
         p->res_lds = static_cast<int>(res_lds);
+        p->res_slot = static_cast<int>(slot_bytes);
         try {
             ranges.resize(static_cast<size_t>(res_ranges) + 1);
         } catch (const std::bad_alloc&) {
@@ -448,8 +493,11 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     if (ok && p->schedule == FC_SCHED_TWO_PASS && p->extent > 0)
         ok = hipMalloc(&p->d_sum, static_cast<size_t>(p->extent) * sizeof(float)) == hipSuccess;
     if (ok && resident) {
+        const size_t clock_bytes = static_cast<size_t>(res_grid) * fc::RESIDENT_CLOCK_WORDS * sizeof(unsigned long long);
         ok = hipMalloc(reinterpret_cast<void**>(&p->d_ranges), ranges.size() * sizeof(int)) == hipSuccess &&
-             hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) == hipSuccess;
+             hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) == hipSuccess &&
+             hipMalloc(reinterpret_cast<void**>(&p->d_clock), clock_bytes) == hipSuccess &&
+             clear_clock(p) == hipSuccess;
         if (ok) {
             // the attribute belongs to the kernel, not to the plan: allow the
             // compute unit's whole LDS, so that no plan lowers another's limit
@@ -500,6 +548,71 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
         info->grid = p->res_grid;
         info->block_threads = 64 * fc::RESIDENT_WAVES;
     }
+    return FC_OK;
+}
+
+int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
+    if (!p || n_rate < 0 || (n_rate > 0 && !xcd_rate)) return FC_EINVAL;
+    for (int i = 0; i < n_rate; ++i) xcd_rate[i] = 0.0f;
+    if (p->schedule != FC_SCHED_RESIDENT) return FC_OK;
+    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess)
+        return FC_EHIP;
+    const int G = p->res_grid, R = p->res_rounds;
+    std::vector<unsigned long long> c;
+    std::vector<int> xcd;
+    std::vector<double> w;
+    std::vector<int> ranges;
+    try {
+        c.resize(static_cast<size_t>(G) * fc::RESIDENT_CLOCK_WORDS);
+        xcd.resize(static_cast<size_t>(G));
+        w.resize(static_cast<size_t>(G));
+    } catch (const std::bad_alloc&) {
+        return FC_ENOMEM;
+    }
+    if (hipMemcpy(c.data(), p->d_clock, c.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost) != hipSuccess)
+        return FC_EHIP;
+    // tiles per tick of the reduce phase, per XCD, over every launch recorded
+    constexpr int NX = 16;  // XCC_ID is 4 bits
+    double tiles[NX] = {}, ticks[NX] = {};
+    double all_tiles = 0.0, all_ticks = 0.0;
+    for (int b = 0; b < G; ++b) {
+        const unsigned long long* cb = &c[static_cast<size_t>(b) * fc::RESIDENT_CLOCK_WORDS];
+        const int x = static_cast<int>(cb[2] & (NX - 1));
+        xcd[b] = x;
+        if (cb[0] > 0 && cb[1] > 0) {
+            tiles[x] += static_cast<double>(cb[0]);
+            ticks[x] += static_cast<double>(cb[1]);
+            all_tiles += static_cast<double>(cb[0]);
+            all_ticks += static_cast<double>(cb[1]);
+        }
+    }
+    if (all_ticks <= 0.0) return FC_OK;  // nothing launched since the plan was made or last balanced
+    const double mean = all_tiles / all_ticks;
+    double rel[NX];
+    for (int x = 0; x < NX; ++x) rel[x] = ticks[x] > 0.0 ? tiles[x] / ticks[x] / mean : 1.0;
+    // shares proportional to the XCD's rate, drawn toward equal shares until
+    // every block's tiles fit its LDS; equal shares always fit
+    bool fit = false;
+    for (double lam = 1.0; lam >= 1.0 / 64; lam *= 0.5) {
+        for (int b = 0; b < G; ++b) w[b] = 1.0 + lam * (rel[xcd[b]] - 1.0);
+        try {
+            if (static_cast<int64_t>(resident_ranges(p->ntiles, R, G, w, ranges)) * p->res_slot <= p->res_lds) {
+                fit = true;
+                break;
+            }
+        } catch (const std::bad_alloc&) {
+            return FC_ENOMEM;
+        }
+    }
+    if (!fit) {
+        const size_t n = static_cast<size_t>(G) * R;
+        for (size_t i = 0; i <= n; ++i) ranges[i] = static_cast<int>(static_cast<uint64_t>(p->ntiles) * i / n);
+    }
+    if (hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) != hipSuccess ||
+        clear_clock(p) != hipSuccess)
+        return FC_EHIP;
+    p->res_ranges.swap(ranges);
+    for (int x = 0; x < n_rate && x < NX; ++x) xcd_rate[x] = ticks[x] > 0.0 ? static_cast<float>(rel[x]) : 0.0f;
     return FC_OK;
 }
 

@@ -574,7 +574,10 @@ __global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ?
 // the store of the raw sum).  In round r the blocks' ranges are neighbours,
 // so the whole grid streams one region of the parameters at a time.  Blocks
 // share nothing, so the result does not depend on how many of them are
-// resident at once.
+// resident at once, nor on how the ranges divide the tiles.  Each block
+// records how long its phase 1 took and on which XCD: blocks on some XCDs
+// read more slowly than on others (measured on MI355X: 6-10%), and the host
+// can give each block a share of tiles in proportion to its XCD's rate.
 template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE>
 __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
     // 16-byte aligned, so that a lane's 4 sums move as one 16-byte LDS access
@@ -586,6 +589,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
     const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const uint32_t lane = threadIdx.x & 63;
     for (int round = 0; round < ra.rounds; ++round) {
+        const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
         const int b = static_cast<int>(blockIdx.x) + round * static_cast<int>(gridDim.x);
         const int lo = ldc(ra.ranges, b);
         const int hi = ldc(ra.ranges, b + 1);
@@ -615,6 +619,15 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
             }
         }
         __syncthreads();
+        if (threadIdx.x == 0) {
+            // how long this block's share took on its XCD (hardware register
+            // XCC_ID, bits 3:0); only this block touches its entry, and
+            // launches of a plan never overlap
+            unsigned long long* c = ra.clock + RESIDENT_CLOCK_WORDS * blockIdx.x;
+            c[0] += static_cast<unsigned long long>(hi - lo);
+            c[1] += __builtin_amdgcn_s_memrealtime() - t0;
+            c[2] = static_cast<unsigned long long>(__builtin_amdgcn_s_getreg((3 << 11) | 20));
+        }
         const int n = (hi - lo) * 64;
         for (int e = static_cast<int>(threadIdx.x); e < n; e += 64 * W) {
             const int j = __builtin_amdgcn_readfirstlane(e / 64);  // one tile per wave

@@ -61,7 +61,13 @@ struct ResidentArgs {
     ReduceArgs r;
     const int* ranges;            // gridDim.x * rounds + 1 tile indices
     int rounds;
+    // per block b, summed over the launches since the host last cleared it:
+    // clock[4b] = tiles reduced, clock[4b + 1] = 10 ns ticks (s_memrealtime,
+    // 100 MHz) of the reduce phase; clock[4b + 2] = the XCD (XCC_ID) the
+    // block last ran on.  Read by the host to balance the ranges.
+    unsigned long long* clock;
 };
+constexpr int RESIDENT_CLOCK_WORDS = 4;
 constexpr int RESIDENT_SLOT = 256;  // floats per tile of 64 lanes x one 4-element vector
 constexpr int RESIDENT_WAVES = 16;
 

@@ -1,7 +1,7 @@
 /* A plain C client of the library's ABI (include/fc.h), with no Python and
  * no torch: it allocates device buffers with the HIP runtime's C API, runs
- * one fc_step and one fc_tree_reduce per schedule on a small ragged segment
- * table, and compares every element bit for bit with the oracle's C
+ * one fc_step, fc_plan_balance and one fc_tree_reduce per schedule on a small
+ * ragged segment table, and compares every element bit for bit with the oracle's C
  * functions (the oracle is linked as test infrastructure) on the same
  * inputs.  Exit status 0 when everything matches; each failure is printed. */
 #include <hip/hip_runtime_api.h>
@@ -108,6 +108,10 @@ int main(void) {
         HIP_OK(hipMemcpy(d_w, w0, sizeof(float) * N, hipMemcpyHostToDevice));
         HIP_OK(hipMemcpy(d_v, v0, sizeof(float) * N, hipMemcpyHostToDevice));
         rc = fc_step(plan, dev_rows, d_w, d_v, lr, mu, wd, batch, NULL, NULL, NULL);
+        /* XCD-aware shares from the step's record (resident plans; a no-op
+           for the others): the reduce that follows runs on the new shares */
+        float rates[16];
+        if (rc == FC_OK) rc = fc_plan_balance(plan, NULL, rates, 16);
         if (rc == FC_OK) rc = fc_tree_reduce(plan, dev_rows, d_out, NULL);
         if (rc != FC_OK) {
             fprintf(stderr, "c client: schedule %d: %s\n", schedules[si], fc_strerror(rc));

@@ -60,9 +60,10 @@ def run_reduce(plan_mod, segs, K, dtype, order, rng, opts=None, special=False, s
 
 
 def run_steps(plan_mod, segs, K, dtype, order, rng, steps=3, opts=None, with_out=False, with_bcast=False,
-              special=False, batch=256):
+              special=False, batch=256, after_step=None):
     """`steps` chained fc_step calls (new replicas each step) vs the oracle;
-    returns the total number of mismatching elements over w, v, out, bcast."""
+    returns the total number of mismatching elements over w, v, out, bcast.
+    after_step(plan), when given, runs after every step."""
     import torch
     npdt = np.float16 if dtype == "f16" else np.float32
     n = alloc_len(segs)
@@ -86,5 +87,7 @@ def run_steps(plan_mod, segs, K, dtype, order, rng, steps=3, opts=None, with_out
         if with_bcast:
             got = dst_d.cpu().numpy()
             bad += sum(same_bits(got[k], dst_h[k]) for k in range(K))
+        if after_step is not None:
+            after_step(plan)
     plan.close()
     return bad

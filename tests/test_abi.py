@@ -26,7 +26,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("fc_plan_create", "fc_plan_create_ex", "fc_plan_destroy", "fc_tree_reduce", "fc_sgd_step",
               "fc_broadcast", "fc_step", "fc_strerror", "fc_plan_query", "fc_plan_set_timing",
-              "fc_plan_read_timing"):
+              "fc_plan_read_timing", "fc_plan_balance"):
         assert n in names
 
 
@@ -99,6 +99,9 @@ def test_null_arguments(fcmod):
     assert f.lib.fc_plan_query(None, None) == f.FC_EINVAL
     assert f.lib.fc_plan_set_timing(None, 1) == f.FC_EINVAL
     assert f.lib.fc_plan_read_timing(None, None) == f.FC_EINVAL
+    rates = (ctypes.c_float * 4)(1, 1, 1, 1)
+    assert f.lib.fc_plan_balance(None, None, rates, 4) == f.FC_EINVAL
+    assert f.lib.fc_plan_balance(None, None, None, 0) == f.FC_EINVAL
     f.fc_plan_destroy(None)
 
 

@@ -213,8 +213,9 @@ def test_schedule_resolution(fc):
         assert (info.schedule, info.scratch_bytes, info.rounds) == (3, 0, 1), (K, dtype)
         assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
         # 3 tiles of 256 elements and one of 232, then the 5-element segment's
-        # vector and its tail tile: one tile per block, 1 KiB of LDS each
-        assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 1024)
+        # vector and its tail tile: one tile per block; LDS for the 6 tiles a
+        # block could be given (fc_plan_balance), 1 KiB each
+        assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 6 * 1024)
     # 160 tiles per block fill 160 KiB of LDS: 256-element tiles for cus * 160 tiles fit
     fits = [(0, cus * 160 * 256, 1, 1)]
     big = [(0, cus * 160 * 256 + 4, 1, 1)]
@@ -240,8 +241,7 @@ def test_schedule_resolution(fc):
     assert fc.Plan(big, 64, "f32", "tree", block_threads=64).info().schedule == 1
     assert fc.Plan(big, 65, "f32", "tree", block_threads=64).info().schedule == 2
     info = fc.Plan(big, 8, "f32", "tree", schedule=3).info()
-    assert (info.schedule, info.rounds) == (3, 2)
-    assert info.lds_bytes == (cus * 160 + 1 + 2 * cus - 1) // (2 * cus) * 1024
+    assert (info.schedule, info.rounds, info.lds_bytes) == (3, 2, 160 * 1024)
 
 
 def test_timing_records_every_launch(fc):
@@ -480,7 +480,7 @@ def test_resident_plans_with_different_lds_interleave(fc):
     rng = np.random.default_rng(77)
     big = fc.Plan(rows_big, K, "f32", "tree", schedule=3)
     small = fc.Plan(rows_small, K, "f32", "tree", schedule=3)
-    assert big.info().lds_bytes == 150 * 1024 and small.info().lds_bytes == 1024
+    assert big.info().lds_bytes == 160 * 1024 and small.info().lds_bytes == 12 * 1024
     reps = torch.from_numpy(rng.standard_normal((K, big_n), dtype=np.float32)).cuda()
     out = torch.full((big_n,), -1.0, device="cuda")
     big.tree_reduce(reps, out)
@@ -511,9 +511,11 @@ def test_batch_not_a_power_of_two(fc, batch):
                                                  (300_000, 8, 3, 1), (1, 1, 0, 1)])
 def test_resident_partition(fc, n, K, max_blocks, vecs):
     """The resident plan's grid, rounds and LDS per block follow from the tile
-    count and the CU's LDS: rounds = ceil(tiles / (grid * slots)), each of the
-    grid * rounds ranges holds at most ceil(tiles / (grid * rounds)) tiles of
-    64 * vecs vectors, each with 1 KiB * vecs of LDS (160 KiB per CU)."""
+    count and the CU's LDS: rounds = ceil(tiles / (grid * slots)) for tiles of
+    64 * vecs vectors, each with 1 KiB * vecs of LDS (160 KiB per CU); a
+    block's LDS holds the slots of as many tiles as it could be given in one
+    round (a round's tiles, at most the CU's slots), so that rebalanced
+    ranges never need more."""
     import math
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -525,7 +527,7 @@ def test_resident_partition(fc, n, K, max_blocks, vecs):
     grid = min(grid, tiles)
     slots = (160 * 1024) // (1024 * vecs)
     rounds = max(1, math.ceil(tiles / (grid * slots)))
-    per = math.ceil(tiles / (grid * rounds))
+    per = min(slots, max(1, math.ceil(tiles / rounds)))
     assert (info.ntiles, info.grid, info.rounds, info.lds_bytes) == (tiles, grid, rounds, per * 1024 * vecs), \
         (info.ntiles, info.grid, info.rounds, info.lds_bytes)
     assert info.lds_bytes <= 160 * 1024
@@ -558,3 +560,106 @@ def test_sharded_reduction_equals_full_tree(fc, K, S):
     q.close()
     torch.cuda.synchronize()
     assert same_bits(top.cpu().numpy(), full.cpu().numpy()) == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("K,max_blocks,vecs", [(16, 0, 1), (33, 0, 1), (5, 1, 1), (64, 3, 1), (40, 2, 2)])
+def test_balance_keeps_bits(fc, K, max_blocks, vecs, dtype):
+    """fc_plan_balance after every step re-divides the resident tiles among
+    the blocks by their XCDs' measured rates: every step before and after
+    stays bit-exact with the oracle (update and raw sum), in one round and in
+    several (1-3 blocks of 160 tile slots)."""
+    segs = table(16000 + K, dtype, nseg=9)
+    if max_blocks:  # enough tiles for several rounds of 1-3 blocks
+        segs = segs + [(alloc_len(segs), 150000, 1.0, 1.0)]
+    opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    p = fc.Plan(segs, K, dtype, "tree", **opts)
+    info = p.info()
+    assert p.balance() == [0.0] * 16  # nothing launched yet: no change, no rates
+    p.close()
+    if max_blocks:
+        assert info.rounds >= 2 and info.grid == max_blocks
+    rates = []
+    bad = run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(K), steps=4, opts=opts, with_out=True,
+                    after_step=lambda plan: rates.append(plan.balance()))
+    assert bad == 0
+    ran = [r for r in rates[-1] if r > 0]
+    assert 1 <= len(ran) <= min(8, info.grid)
+
+
+def test_balance_full_grid_reduce(fc):
+    """One round over the whole grid (every XCD): the raw sums before and
+    after rebalancing are the same bits, equal to the pairwise tree of 4."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = cus * 120 * 256 + 13
+    K = 4
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((K, n + 3), dtype=np.float32)
+    reps = to_dev(x)
+    plan = fc.Plan([(0, n, 1.0, 1.0)], K, "f32", "tree", schedule=3)
+    assert plan.info().rounds == 1 and plan.info().grid == cus
+    out = torch.full((n + 3,), -1.0, device="cuda")
+    plan.tree_reduce(reps, out)
+    rates = plan.balance()
+    assert sum(1 for r in rates if r > 0) == min(8, cus)
+    first = out.cpu().numpy()
+    out.fill_(-1.0)
+    for _ in range(3):
+        plan.tree_reduce(reps, out)
+        plan.balance()
+    torch.cuda.synchronize()
+    expect = (x[0] + x[1]) + (x[2] + x[3])
+    expect[n:] = -1.0
+    assert same_bits(first, expect) == 0
+    assert same_bits(out.cpu().numpy(), expect) == 0
+    plan.close()
+
+
+def test_balance_leaves_other_schedules(fc):
+    segs = table(17000, "f32", nseg=4)
+    p = fc.Plan(segs, 8, "f32", "tree", schedule=1)
+    rng = np.random.default_rng(3)
+    n = alloc_len(segs)
+    reps = to_dev(host_replicas(rng, 8, n, np.float32))
+    w, v = to_dev(np.zeros(n, np.float32)), to_dev(np.zeros(n, np.float32))
+    p.step(reps, w, v, LR, MU, WD, 256)
+    assert p.balance() == [0.0] * 16
+    p.close()
+
+
+def test_graph_replays_after_balance(fc):
+    """A graph captured before fc_plan_balance replays with the new shares
+    (the range table changes in place; the launches' LDS already covers any
+    share), bit-identical to an eager twin plan."""
+    import torch
+    segs = table(18000, "f32", nseg=9)
+    K = 24
+    n = alloc_len(segs)
+    rng = np.random.default_rng(11)
+    reps = to_dev(host_replicas(rng, K, n, np.float32, scale=0.01))
+    w0 = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+    wa, va = to_dev(w0), torch.zeros(n, device="cuda")
+    wb, vb = to_dev(w0), torch.zeros(n, device="cuda")
+    pa = fc.Plan(segs, K, "f32", "tree", schedule=3)
+    pb = fc.Plan(segs, K, "f32", "tree", schedule=3)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+    s.synchronize()
+    pb.step(reps, wb, vb, LR, MU, WD, 256)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+    for _ in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        pa.balance(stream=s)
+        pb.step(reps, wb, vb, LR, MU, WD, 256)
+        torch.cuda.synchronize()
+        assert same_bits(wa.cpu().numpy(), wb.cpu().numpy()) == 0
+        assert same_bits(va.cpu().numpy(), vb.cpu().numpy()) == 0
+    pa.close()
+    pb.close()
