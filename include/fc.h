@@ -305,7 +305,7 @@ int fc_plan_read_timing(fc_plan* plan, fc_timing* timing);
  * balanced, clears it, and re-divides every round's tiles so that each
  * block's share is proportional to the tiles per second measured on its XCD,
  * drawn toward equal shares as far as needed for every share to fit a
- * block's LDS.  Only which block
+ * block's LDS.  The stream of the plan's last call is drained too.  Only which block
  * reduces a tile changes: results are bit-identical before and after.  The
  * new shares apply to every later launch, including launches of graphs
  * captured before (the plan's device tables change in place; their sizes

@@ -555,7 +555,11 @@ int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
     if (!p || n_rate < 0 || (n_rate > 0 && !xcd_rate)) return FC_EINVAL;
     for (int i = 0; i < n_rate; ++i) xcd_rate[i] = 0.0f;
     if (p->schedule != FC_SCHED_RESIDENT) return FC_OK;
-    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess)
+    // no launch of this plan may still read the range table or write the
+    // record: drain the given stream and the stream of the plan's last call
+    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess ||
+        (p->have_last_stream && p->last_stream != static_cast<hipStream_t>(stream) &&
+         hipStreamSynchronize(p->last_stream) != hipSuccess))
         return FC_EHIP;
     const int G = p->res_grid, R = p->res_rounds;
     std::vector<unsigned long long> c;

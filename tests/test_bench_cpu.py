@@ -1,0 +1,61 @@
+"""bench.py's parts that need no GPU: the one-GPU contract, the kernel-source
+hash that ties profiles/ to the sources, and the algorithmic byte counts the
+roofline entry divides by."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+
+def run_bench(*args):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                          cwd=ROOT, timeout=120)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = run_bench("--gpus", "2")
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_kernel_hash_is_stable_and_ignores_comments(tmp_path, monkeypatch):
+    import bench
+    h = bench.kernel_hash()
+    assert len(h) == 16 and h == bench.kernel_hash()
+    assert run_bench("--print-hash").stdout.strip() == h
+    src = "int f(int x) { // a comment\n  return x; /* another */ }\n"
+    assert bench._code_tokens(src) == bench._code_tokens("int f(int x) {\n return x;  }")
+    assert bench._code_tokens(src) != bench._code_tokens("int f(int x) { return x + 1; }")
+
+
+@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "vgg19", "alexnet"])
+def test_kernel_bytes_match_the_workload(name):
+    import bench
+    from workloads import tables
+    wl = tables.get(name)
+    n, K, sg = wl.n_params, wl.K, wl.s_g
+    assert bench.kernel_bytes(wl, "step") == wl.algorithmic_bytes() == n * (K * sg + 16)
+    assert bench.kernel_bytes(wl, "step", out=True) == wl.algorithmic_bytes(out=True) == n * (K * sg + 20)
+    assert bench.kernel_bytes(wl, "step", bcast=True) == wl.algorithmic_bytes(bcast=True) == n * (K * sg + 16 + 4 * K)
+    # the two passes of the two-pass schedule add up to the step plus the raw sum written and read back
+    assert bench.kernel_bytes(wl, "reduce") + bench.kernel_bytes(wl, "sgd") == n * (K * sg + 16) + 8 * n
+
+
+def test_traffic_profiles_name_their_kernel_and_bytes():
+    """Every committed traffic summary states its workload, kernel, the source
+    hash it was taken on and HBM bytes within 1% of the algorithmic bytes."""
+    for name in ("flat", "nin", "googlenet", "vgg19", "alexnet"):
+        kv = {}
+        with open(os.path.join(ROOT, "profiles", f"traffic_{name}.txt")) as f:
+            for line in f:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        assert kv["workload"] == name and kv["kernel"] == "step"
+        assert len(kv["kernel_source_sha256_16"]) == 16
+        ratio = float(kv["hbm_bytes_per_step"]) / float(kv["algorithmic_bytes_per_step"])
+        assert 0.99 < ratio < 1.01, (name, ratio)

@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 from gpu_cases import LR, MU, WD, alloc_len, host_replicas, run_reduce, run_steps, same_bits, to_dev
+import oracle
 from workloads import gen
 
 pytestmark = pytest.mark.gpu
@@ -663,3 +664,30 @@ def test_graph_replays_after_balance(fc):
         assert same_bits(va.cpu().numpy(), vb.cpu().numpy()) == 0
     pa.close()
     pb.close()
+
+
+def test_balance_drains_the_plans_stream(fc):
+    """Steps on a side stream, fc_plan_balance called with the null stream:
+    the call drains the stream the plan last ran on before it replaces the
+    range table, and every later step stays bit-exact."""
+    import torch
+    segs = table(19000, "f32", nseg=9)
+    K = 20
+    n = alloc_len(segs)
+    rng = np.random.default_rng(12)
+    reps_h = host_replicas(rng, K, n, np.float32, scale=0.01)
+    w = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+    v = np.zeros(n, np.float32)
+    p = fc.Plan(segs, K, "f32", "tree", schedule=3)
+    reps, w_d, v_d = to_dev(reps_h), to_dev(w), to_dev(v)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    for i in range(4):
+        with torch.cuda.stream(side):
+            p.step(reps, w_d, v_d, LR, MU, WD, 256)
+        w, v, _, _ = oracle.step(segs, list(reps_h), w, v, LR, MU, WD, 256)
+        rates = p.balance(stream=0)
+        assert any(r > 0 for r in rates)
+    side.synchronize()
+    assert same_bits(w_d.cpu().numpy(), w) == 0 and same_bits(v_d.cpu().numpy(), v) == 0
+    p.close()
