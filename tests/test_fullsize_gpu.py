@@ -1,11 +1,14 @@
 """Parity at the full workload sizes, in the launch configuration bench.py
-times (the plan defaults), on sampled outputs the oracle computes one by one.
+times (the plan defaults, resident shares rebalanced per XCD after the first
+step as bench.py does after its warm-up), on sampled outputs the oracle
+computes one by one.
 
 For each of the five workloads (flat 2^20 x K=4, NiN x K=32, GoogLeNet
 x K=128, VGG-19 x K=16, AlexNet fp16 x K=128) the inputs are drawn on the
-device, two fused steps run on the GPU, and at every segment's first, second,
-last and one random element plus 1500 random elements the oracle recomputes
-the same two steps from the gathered inputs; w' and v' must match bit for bit.
+device, three fused steps run on the GPU (fc_plan_balance after the first),
+and at every segment's first, second, last and one random element plus 1500
+random elements the oracle recomputes the same three steps from the gathered
+inputs; w' and v' must match bit for bit.
 A property that holds at any size is checked on the whole buffer: the fused
 step equals reduce, then SGD, then (for GoogLeNet) nothing else differs.
 """
@@ -55,8 +58,10 @@ def test_fullsize_sampled(fc, name):
     g_s = reps[:, it].cpu().numpy()                 # (K, S) gathered replica values
     w_s, v_s = w[it].cpu().numpy(), v[it].cpu().numpy()
     plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
-    for _ in range(2):
+    for i in range(3):
         plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
+        if i == 0:
+            plan.balance()
     torch.cuda.synchronize()
     got_w, got_v = w[it].cpu().numpy(), v[it].cpu().numpy()
     plan.close()
@@ -67,14 +72,15 @@ def test_fullsize_sampled(fc, name):
     js = segment_of(wl, idx)
     rows = [(i, 1, wl.segments[j].lr_mult, wl.segments[j].decay_mult) for i, j in enumerate(js)]
     ew, ev = w_s, v_s
-    for _ in range(2):
+    for _ in range(3):
         ew, ev, _, _ = oracle.step(rows, list(g_s), ew, ev, wl.lr, wl.mu, wl.wd, wl.batch)
     assert same_bits(got_w, ew) == 0 and same_bits(got_v, ev) == 0
 
 
 def test_fullsize_fused_equals_composed(fc):
     """At full GoogLeNet size: one fused step == tree reduce, then SGD, on the
-    whole buffer (a property independent of the oracle)."""
+    whole buffer (a property independent of the oracle), with the resident
+    shares rebalanced per XCD between the fused step and the other two."""
     import torch
     wl = tables.googlenet()
     dev = torch.device("cuda:0")
@@ -84,6 +90,7 @@ def test_fullsize_fused_equals_composed(fc):
     g = torch.zeros_like(w)
     plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
     plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
+    assert sum(1 for r in plan.balance() if r > 0) == 8
     plan.tree_reduce(reps, g)
     plan.sgd_step(w2, v2, g, wl.lr, wl.mu, wl.wd, wl.batch)
     torch.cuda.synchronize()
@@ -96,9 +103,10 @@ def test_fullsize_fused_equals_composed(fc):
 def test_offsets_beyond_4gib(fc, dtype, schedule):
     """A segment of 2^31 + 100 elements: element indices pass 2^31 and byte
     offsets pass 4 GiB (8 GiB of fp32) in every buffer, the tile map holds
-    8.4 M tiles and the resident schedule takes about 200 rounds.  Windows at
-    the start, around element 2^31 and at the end are recomputed by the oracle
-    from the gathered inputs (elements are independent within a segment)."""
+    8.4 M tiles and the resident schedule takes about 200 rounds, rebalanced
+    per XCD between the two steps.  Windows at the start, around element 2^31
+    and at the end are recomputed by the oracle from the gathered inputs
+    (elements are independent within a segment)."""
     import torch
     dev = torch.device("cuda:0")
     big = (1 << 31) + 100
@@ -121,11 +129,15 @@ def test_offsets_beyond_4gib(fc, dtype, schedule):
     if schedule == 3:
         assert plan.info().rounds > 100
     plan.step(reps, w, v, 0.01, 0.9, 5e-4, 256)
+    plan.balance()
+    plan.step(reps, w, v, 0.01, 0.9, 5e-4, 256)
     torch.cuda.synchronize()
     plan.close()
     for (a, b), (r_h, w_h, v_h) in zip(wins, before):
         seg = [r for r in rows if r[0] <= a < r[0] + r[1]][0]
-        ew, ev, _, _ = oracle.step([(0, b - a, seg[2], seg[3])], list(r_h), w_h, v_h, 0.01, 0.9, 5e-4, 256)
+        ew, ev = w_h, v_h
+        for _ in range(2):
+            ew, ev, _, _ = oracle.step([(0, b - a, seg[2], seg[3])], list(r_h), ew, ev, 0.01, 0.9, 5e-4, 256)
         assert same_bits(w[a:b].cpu().numpy(), ew) == 0, (a, b)
         assert same_bits(v[a:b].cpu().numpy(), ev) == 0, (a, b)
     del reps, w, v
