@@ -313,8 +313,11 @@ int fc_plan_read_timing(fc_plan* plan, fc_timing* timing);
  * plan on another stream.
  * xcd_rate (nullable): n_rate floats, entry x = XCD x's measured rate relative
  * to the mean over all blocks, 0 for an XCD that ran no block (at most 16 XCDs
- * are reported).  A plan that is not RESIDENT, or has not launched since it
- * was made or last balanced, is left as it is (FC_OK, rates 0).  Errors: FC_EINVAL (NULL plan,
+ * are reported).  A plan that is not RESIDENT, whose blocks take fewer than
+ * 32 tiles (of 256 elements) per round -- a launch of a few microseconds,
+ * where the record would cost more than balancing gains, so nothing is
+ * recorded -- or that has not launched since it was made or last balanced,
+ * is left as it is (FC_OK, rates 0).  Errors: FC_EINVAL (NULL plan,
  * n_rate < 0, or n_rate > 0 with xcd_rate NULL), FC_EHIP, FC_ENOMEM. */
 int fc_plan_balance(fc_plan* plan, void* stream, float* xcd_rate, int n_rate);
 

@@ -42,6 +42,7 @@ struct fc_plan {
     int res_rounds = 0;
     int res_lds = 0;                 // RESIDENT: LDS bytes per block
     int res_slot = 0;                // RESIDENT: LDS bytes per tile
+    bool res_record = false;         // RESIDENT: launches record per-block rates into d_clock
     std::vector<int> res_ranges;     // RESIDENT: host copy of the d_ranges table
     unsigned long long* d_clock = nullptr;  // RESIDENT: per block, the kernel's phase-1 clock and XCD
 
@@ -134,7 +135,7 @@ hipError_t launch_resident(fc_plan* p, int mode, const fc::ReduceArgs& r, hipStr
     fc::ResidentArgs a{};
     a.r = r;
     a.rounds = 1;
-    a.clock = p->d_clock;
+    a.clock = p->res_record ? p->d_clock : nullptr;
     const size_t lds = static_cast<size_t>(p->res_lds);
     for (int round = 0; round < p->res_rounds; ++round) {
         a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
@@ -475,6 +476,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         p->res_rounds = static_cast<int>(res_rounds);
         p->res_lds = static_cast<int>(res_lds);
         p->res_slot = static_cast<int>(slot_bytes);
+        p->res_record = (res_tiles + res_ranges - 1) / res_ranges >= static_cast<uint64_t>(fc::RESIDENT_RECORD_MIN_TILES);
         try {
             ranges.resize(static_cast<size_t>(res_ranges) + 1);
         } catch (const std::bad_alloc&) {
@@ -554,7 +556,7 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
 int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
     if (!p || n_rate < 0 || (n_rate > 0 && !xcd_rate)) return FC_EINVAL;
     for (int i = 0; i < n_rate; ++i) xcd_rate[i] = 0.0f;
-    if (p->schedule != FC_SCHED_RESIDENT) return FC_OK;
+    if (p->schedule != FC_SCHED_RESIDENT || !p->res_record) return FC_OK;
     // no launch of this plan may still read the range table or write the
     // record: drain the given stream and the stream of the plan's last call
     if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess ||

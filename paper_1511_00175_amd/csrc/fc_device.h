@@ -589,7 +589,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
     const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const uint32_t lane = threadIdx.x & 63;
     for (int round = 0; round < ra.rounds; ++round) {
-        const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+        const unsigned long long t0 = ra.clock ? __builtin_amdgcn_s_memrealtime() : 0ull;
         const int b = static_cast<int>(blockIdx.x) + round * static_cast<int>(gridDim.x);
         const int lo = ldc(ra.ranges, b);
         const int hi = ldc(ra.ranges, b + 1);
@@ -619,13 +619,15 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
             }
         }
         __syncthreads();
-        if (threadIdx.x == 0) {
+        if (threadIdx.x == 0 && ra.clock) {
             // how long this block's share took on its XCD (hardware register
-            // XCC_ID, bits 3:0); only this block touches its entry, and
-            // launches of a plan never overlap
+            // XCC_ID, bits 3:0); only this block touches its entry, and the
+            // adds return nothing, so the wave goes on at once
             unsigned long long* c = ra.clock + RESIDENT_CLOCK_WORDS * blockIdx.x;
-            c[0] += static_cast<unsigned long long>(hi - lo);
-            c[1] += __builtin_amdgcn_s_memrealtime() - t0;
+            __hip_atomic_fetch_add(c, static_cast<unsigned long long>(hi - lo), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(c + 1, __builtin_amdgcn_s_memrealtime() - t0, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
             c[2] = static_cast<unsigned long long>(__builtin_amdgcn_s_getreg((3 << 11) | 20));
         }
         const int n = (hi - lo) * 64;

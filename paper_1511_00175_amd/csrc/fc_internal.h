@@ -64,7 +64,8 @@ struct ResidentArgs {
     // per block b, summed over the launches since the host last cleared it:
     // clock[4b] = tiles reduced, clock[4b + 1] = 10 ns ticks (s_memrealtime,
     // 100 MHz) of the reduce phase; clock[4b + 2] = the XCD (XCC_ID) the
-    // block last ran on.  Read by the host to balance the ranges.
+    // block last ran on.  Read by the host to balance the ranges; nullptr
+    // when the plan keeps equal shares (nothing is recorded).
     unsigned long long* clock;
 };
 constexpr int RESIDENT_CLOCK_WORDS = 4;

@@ -78,6 +78,15 @@ inline bool default_resident(int K, int bytes_per_element, int64_t rounds) {
     return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 64;
 }
 
+// Resident launches record each block's rate (for fc_plan_balance) when a
+// block's share of a round is at least this many tiles.  Measured on
+// MI355X: the record costs about 0.6 us per launch (the timer read and the
+// adds at the end of the reduce phase), 8% of a flat 2^20 x K=4 step (16
+// tiles per block) and under 0.2% of the NiN-, GoogLeNet-, VGG-19- and
+// AlexNet-sized steps (107-157 tiles per block), where balancing gains up to
+// 1.6%.
+constexpr int RESIDENT_RECORD_MIN_TILES = 32;
+
 // Two passes (reduce into a raw-sum buffer, then update) when a parameter's
 // replicas take more than 256 bytes: HBM serves the replica stream with one
 // write stream far better than with two (measured on MI355X; see fc_schedule).

@@ -564,22 +564,23 @@ def test_sharded_reduction_equals_full_tree(fc, K, S):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("K,max_blocks,vecs", [(16, 0, 1), (33, 0, 1), (5, 1, 1), (64, 3, 1), (40, 2, 2)])
+@pytest.mark.parametrize("K,max_blocks,vecs", [(16, 8, 1), (33, 16, 1), (5, 1, 1), (64, 3, 1), (40, 2, 2)])
 def test_balance_keeps_bits(fc, K, max_blocks, vecs, dtype):
     """fc_plan_balance after every step re-divides the resident tiles among
     the blocks by their XCDs' measured rates: every step before and after
-    stays bit-exact with the oracle (update and raw sum), in one round and in
-    several (1-3 blocks of 160 tile slots)."""
+    stays bit-exact with the oracle (update and raw sum), in one round over
+    8 or 16 blocks (every XCD) and in several rounds (1-3 blocks of 160 tile
+    slots)."""
     segs = table(16000 + K, dtype, nseg=9)
-    if max_blocks:  # enough tiles for several rounds of 1-3 blocks
-        segs = segs + [(alloc_len(segs), 150000, 1.0, 1.0)]
+    segs = segs + [(alloc_len(segs), 150000, 1.0, 1.0)]  # >= 32 tiles per block: launches record
     opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     p = fc.Plan(segs, K, dtype, "tree", **opts)
     info = p.info()
     assert p.balance() == [0.0] * 16  # nothing launched yet: no change, no rates
     p.close()
-    if max_blocks:
-        assert info.rounds >= 2 and info.grid == max_blocks
+    assert info.grid == max_blocks
+    if max_blocks <= 3:
+        assert info.rounds >= 2
     rates = []
     bad = run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(K), steps=4, opts=opts, with_out=True,
                     after_step=lambda plan: rates.append(plan.balance()))
@@ -617,16 +618,20 @@ def test_balance_full_grid_reduce(fc):
     plan.close()
 
 
-def test_balance_leaves_other_schedules(fc):
+def test_balance_leaves_other_schedules_and_small_plans(fc):
+    """Fused plans, and resident plans whose blocks take fewer than 32 tiles
+    per round (here one tile per block), record nothing and keep their
+    shares: fc_plan_balance returns no rates."""
     segs = table(17000, "f32", nseg=4)
-    p = fc.Plan(segs, 8, "f32", "tree", schedule=1)
     rng = np.random.default_rng(3)
     n = alloc_len(segs)
     reps = to_dev(host_replicas(rng, 8, n, np.float32))
     w, v = to_dev(np.zeros(n, np.float32)), to_dev(np.zeros(n, np.float32))
-    p.step(reps, w, v, LR, MU, WD, 256)
-    assert p.balance() == [0.0] * 16
-    p.close()
+    for sched in (1, 3):
+        p = fc.Plan(segs, 8, "f32", "tree", schedule=sched)
+        p.step(reps, w, v, LR, MU, WD, 256)
+        assert p.balance() == [0.0] * 16, sched
+        p.close()
 
 
 def test_graph_replays_after_balance(fc):
@@ -634,7 +639,7 @@ def test_graph_replays_after_balance(fc):
     (the range table changes in place; the launches' LDS already covers any
     share), bit-identical to an eager twin plan."""
     import torch
-    segs = table(18000, "f32", nseg=9)
+    segs = table(18000, "f32", nseg=9)  # 110 tiles, 55 per block of 2: launches record
     K = 24
     n = alloc_len(segs)
     rng = np.random.default_rng(11)
@@ -642,8 +647,8 @@ def test_graph_replays_after_balance(fc):
     w0 = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
     wa, va = to_dev(w0), torch.zeros(n, device="cuda")
     wb, vb = to_dev(w0), torch.zeros(n, device="cuda")
-    pa = fc.Plan(segs, K, "f32", "tree", schedule=3)
-    pb = fc.Plan(segs, K, "f32", "tree", schedule=3)
+    pa = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=2)
+    pb = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=2)
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
@@ -657,7 +662,7 @@ def test_graph_replays_after_balance(fc):
     for _ in range(3):
         g.replay()
         torch.cuda.synchronize()
-        pa.balance(stream=s)
+        assert sum(1 for r in pa.balance(stream=s) if r > 0) == 2
         pb.step(reps, wb, vb, LR, MU, WD, 256)
         torch.cuda.synchronize()
         assert same_bits(wa.cpu().numpy(), wb.cpu().numpy()) == 0
@@ -678,7 +683,7 @@ def test_balance_drains_the_plans_stream(fc):
     reps_h = host_replicas(rng, K, n, np.float32, scale=0.01)
     w = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
     v = np.zeros(n, np.float32)
-    p = fc.Plan(segs, K, "f32", "tree", schedule=3)
+    p = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=2)  # 106 tiles: 53 per block, launches record
     reps, w_d, v_d = to_dev(reps_h), to_dev(w), to_dev(v)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
