@@ -104,9 +104,10 @@ typedef struct fc_plan fc_plan;
  *   makes fc_tree_reduce store the sums only after each read phase.  Tiles of
  *   64 lanes x 1 vector with batches of 16 replicas (default), or x 2 vectors
  *   with batches of 4 (vecs_per_thread 2, K < 512); no K split.
- * AUTO (no launch-shape field given): RESIDENT when one round holds the plan
- *   or a parameter's replicas take at least 64 bytes (K * bytes per element),
- *   else FUSED.  With a launch-shape field: TWO_PASS when they take more than
+ * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
+ *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
+ *   round holds the plan or a parameter's replicas take at least 64 bytes
+ *   (K * bytes per element), else FUSED.  With a launch-shape field: TWO_PASS when they take more than
  *   256 bytes, else FUSED. */
 typedef enum {
     FC_SCHED_AUTO = 0,

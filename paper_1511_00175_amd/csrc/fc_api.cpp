@@ -389,10 +389,13 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     const uint64_t res_lds =
         std::min<uint64_t>(cap, std::max<uint64_t>(1, (res_tiles + res_rounds - 1) / res_rounds)) * slot_bytes;
     if (res_ranges > static_cast<uint64_t>(INT32_MAX) - 1) return FC_EINVAL;
+    // algorithmic bytes of one step (saturating)
+    const uint64_t per_elem = static_cast<uint64_t>(K) * (gdt == FC_F16 ? 2 : 4) + 16;
+    const uint64_t step_bytes = n_elems > UINT64_MAX / per_elem ? UINT64_MAX : n_elems * per_elem;
     const bool resident =
         sched_req == FC_SCHED_RESIDENT ||
         (sched_req == FC_SCHED_AUTO && !shape_given &&
-         fc::default_resident(K, gdt == FC_F16 ? 2 : 4, static_cast<int64_t>(res_rounds)));
+         fc::default_resident(K, gdt == FC_F16 ? 2 : 4, static_cast<int64_t>(res_rounds), step_bytes));
     if (resident) {
         sh.block = 64;
         sh.vecs = res_u;

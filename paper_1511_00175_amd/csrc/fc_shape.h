@@ -74,7 +74,17 @@ inline bool compiled_pair(int u, int c) {
 // K=32/64 1431/2553 vs 1473/2810 (6 rounds); below 64 bytes the fused kernel
 // wins (VGG-19 K=8 1213 vs 1203, K=4 846 vs 766; AlexNet fp16 K=16 521 vs
 // 517), its update writes being a larger share of the bytes.
-inline bool default_resident(int K, int bytes_per_element, int64_t rounds) {
+// Steps of less than RESIDENT_MIN_BYTES of algorithmic traffic (a few
+// microseconds of HBM time) stay on the single-pass fused kernel, whose one
+// round trip to memory beats the resident kernel's two phases: measured on
+// MI355X, us per step in a HIP graph, fused vs resident: 2^20 x K=4 (33.5 MB)
+// 5.2 vs 6.6, 60000 x K=128 (31 MB) 9.5 vs 10.1, 1000 x K=1024 36.8 vs 39.1;
+// from 84 MB up the resident kernel is as fast or faster (2^20 x K=16 13.0
+// vs 15.0, fp16 2^20 x K=64 24.1 vs 26.4, 2^21 x K=8 15.2 vs 15.6, 200000 x
+// K=256 34.4 vs 34.2).
+constexpr uint64_t RESIDENT_MIN_BYTES = uint64_t(64) << 20;
+inline bool default_resident(int K, int bytes_per_element, int64_t rounds, uint64_t step_bytes) {
+    if (step_bytes < RESIDENT_MIN_BYTES) return false;
     return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 64;
 }
 

@@ -203,14 +203,23 @@ def test_schedules_match_oracle(fc, K, schedule, dtype):
 
 
 def test_schedule_resolution(fc):
-    """AUTO takes the resident schedule when every block's share of tiles
-    fits a compute unit's LDS; otherwise two passes when a parameter's
-    replicas exceed 256 bytes, only then with a raw-sum scratch buffer."""
+    """AUTO keeps steps of less than 64 MiB on the fused kernel (two passes
+    when a parameter's replicas exceed 256 bytes); above that it takes the
+    resident schedule when every block's share of tiles fits a compute
+    unit's LDS; otherwise two passes when a parameter's replicas exceed 256
+    bytes, only then with a raw-sum scratch buffer."""
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     small = [(0, 1000, 1, 1), (1024, 5, 1, 1)]
-    for K, dtype in ((1, "f32"), (64, "f32"), (1024, "f32"), (129, "f16")):
+    for K, dtype, sched in ((1, "f32", 1), (64, "f32", 1), (65, "f32", 2), (1024, "f32", 2), (128, "f16", 1),
+                            (129, "f16", 2)):
         info = fc.Plan(small, K, dtype, "tree").info()
+        assert (info.schedule, info.rounds) == (sched, 0), (K, dtype)
+    # 2^20 x K=4 fp32 (32 MiB of replicas + 16 MiB of w, v): fused; K=16 (80 MiB): resident
+    assert fc.Plan([(0, 1 << 20, 1, 1)], 4, "f32", "tree").info().schedule == 1
+    assert fc.Plan([(0, 1 << 20, 1, 1)], 16, "f32", "tree").info().schedule == 3
+    for K, dtype in ((1, "f32"), (64, "f32"), (1024, "f32"), (129, "f16")):
+        info = fc.Plan(small, K, dtype, "tree", schedule=3).info()
         assert (info.schedule, info.scratch_bytes, info.rounds) == (3, 0, 1), (K, dtype)
         assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
         # 3 tiles of 256 elements and one of 232, then the 5-element segment's
