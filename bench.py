@@ -4,10 +4,11 @@
 One step = one fc_step call over all K synthetic gradient replicas of a
 workload (reduce in binary-tree order, average, SGD with momentum and weight
 decay, write back w and v), with every input resident in device memory.  The
-plan's schedule runs the step as one fused kernel or as a reduce pass and an
-update pass (GoogLeNet K=128).  Consecutive steps alternate between two
-independent input sets (--rotate), so that no step is served w and v from the
-previous step's cache lines.
+plan's schedule runs the step as one resident kernel (reduce into LDS, then
+update from it), one fused kernel, or a reduce pass and an update pass.
+Consecutive steps alternate between two independent replica sets (--rotate),
+and w, v rotate over enough sets of their own (--wv-sets) that no step finds
+earlier steps' w and v in the Infinity Cache.
 
 Prints ONE JSON line: effective HBM GB/s of the step (algorithmic bytes per
 step / wall time per step over the timed steps), the roofline entry of the
@@ -31,10 +32,19 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD published peak
-# Two input sets by default: in training, w and v are evicted from the caches
-# by the forward and backward passes between two steps; with one set, part of
-# w and v (56 MB for GoogLeNet) would still sit in the 256 MB Infinity Cache.
+INFINITY_CACHE_BYTES = 256 << 20  # MI355X last-level (memory-side) cache
+# Two replica sets by default, each far larger than the caches.  w and v are
+# rotated over enough sets of their own that their footprint is at least
+# twice the Infinity Cache: measured on MI355X, with up to four (w, v) sets
+# of a GoogLeNet- or NiN-sized plan (56-60 MB each) every step found the
+# previous steps' w and v in that cache (GoogLeNet 533-535 us per step with
+# 1, 2 or 4 sets, 541 with 8; NiN 162-165 vs 168).  In training the forward
+# and backward passes between two steps would evict them.
 DEFAULT_ROTATE = 2
+
+
+def default_wv_sets(wl, rotate):
+    return max(rotate, math.ceil(2 * INFINITY_CACHE_BYTES / (8 * wl.padded)))
 METRIC = "effective HBM GB/s (and % of peak) for tree-reduce+SGD step; µs per step"
 CSRC = os.path.join(ROOT, "paper_1511_00175_amd", "csrc")
 
@@ -246,18 +256,18 @@ def sweep_k(args):
                               "bound_gamma_d": d * u / (1 - d * u)}), flush=True)
 
 
-def input_hash(sets):
+def input_hash(sets, wv):
     """sha256 (first 16 hex digits) over the first and last 4 KiB of every
-    input buffer (each replica row, w, v) of every input set, in order: names
-    the synthetic inputs a run measured."""
+    input buffer (each replica row of every replica set, then w and v of
+    every (w, v) set), in order: names the synthetic inputs a run measured."""
     import torch
 
     h = hashlib.sha256()
-    for reps, w, v in sets:
-        for t in [reps[k] for k in range(reps.shape[0])] + [w, v]:
-            b = t.view(-1).view(dtype=torch.uint8)
-            h.update(b[:4096].cpu().numpy().tobytes())
-            h.update(b[-4096:].cpu().numpy().tobytes())
+    bufs = [reps[k] for reps, _, _ in sets for k in range(reps.shape[0])] + [t for pair in wv for t in pair]
+    for t in bufs:
+        b = t.view(-1).view(dtype=torch.uint8)
+        h.update(b[:4096].cpu().numpy().tobytes())
+        h.update(b[-4096:].cpu().numpy().tobytes())
     return h.hexdigest()[:16]
 
 
@@ -360,8 +370,10 @@ def main():
     ap.add_argument("--no-balance", action="store_true",
                     help="keep equal resident shares (no fc_plan_balance after the warm-up)")
     ap.add_argument("--rotate", type=int, default=DEFAULT_ROTATE,
-                    help="R independent input sets (replicas, w, v), step i using set i mod R, so that no "
-                         "step finds the previous step's w and v in a cache (1: one set)")
+                    help="R independent replica sets, step i using set i mod R (1: one set)")
+    ap.add_argument("--wv-sets", type=int, default=0,
+                    help="W independent (w, v) sets, step i using set i mod W (default: at least R and enough "
+                         "for twice the Infinity Cache, so that no step finds earlier steps' w and v cached)")
     args = ap.parse_args()
 
     if args.print_hash:
@@ -393,9 +405,12 @@ def main():
 
     print(f"# workload {wl.name}: K={wl.K} {wl.dtype} N={wl.n_params} segs={len(wl.segments)}", file=sys.stderr,
           flush=True)
-    if args.rotate < 1:
-        ap.error("--rotate must be >= 1")
+    if args.rotate < 1 or args.wv_sets < 0:
+        ap.error("--rotate must be >= 1 and --wv-sets >= 0")
     sets = [gen.device_inputs(wl, args.seed + 7919 * i, dev) for i in range(args.rotate)]
+    n_wv = args.wv_sets or default_wv_sets(wl, args.rotate)
+    wv = [(ww, vv) for _, ww, vv in sets][:n_wv]
+    wv += [gen.device_weights(wl, args.seed + 7919 * i, dev) for i in range(len(wv), n_wv)]
     reps, w, v = sets[0]
     out = torch.zeros_like(w) if args.out else None
     bcast = torch.zeros((wl.K, wl.padded), device=dev) if args.bcast else None
@@ -409,9 +424,9 @@ def main():
 
     def step():
         i = count[0] % len(sets)
+        ww, vv = wv[count[0] % len(wv)]
         count[0] += 1
-        r, ww, vv = sets[i]
-        plans[i].step(r, ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
+        plans[i].step(sets[i][0], ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
 
     for _ in range(args.warmup):
         step()
@@ -493,7 +508,7 @@ def main():
     avg = kernels[dom]["avg_us"] * 1e-6
     achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
     plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE or
-                 args.no_balance)
+                 args.no_balance or args.wv_sets)
     traffic = read_traffic(wl.name, dom) if plain else None
     sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
     rk = "ksplit_kernel" if info.k_waves > 1 else "resident_kernel" if info.schedule == 3 else "reduce_kernel"
@@ -523,8 +538,9 @@ def main():
                        "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "k_waves": info.k_waves,
                        "schedule": sched, "rounds": info.rounds, "lds_bytes": info.lds_bytes},
             "input_sets": args.rotate,
+            "w_v_sets": n_wv,
             "balance": balance,
-            "input_hash": input_hash(sets),
+            "input_hash": input_hash(sets, wv),
             "step_times": step_times,
             "kernels": kernels,
             "parallelism": "single GPU",

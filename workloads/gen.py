@@ -97,17 +97,36 @@ def device_inputs(wl, seed, device, K=None, stride=None):
         x = torch.randn((K, s.length), generator=g, device=device, dtype=torch.float32)
         reps[:, s.offset:s.offset + s.length] = (x * sig).to(gdt)
         del x
-    g.manual_seed(seed + 1)
+    _draw_weights(wl, seed + 1, g, w)
+    return reps, w, v
+
+
+def _draw_weights(wl, seed, g, w):
+    import torch
+
+    g.manual_seed(seed)
     for s in wl.segments:
         kind, a = weight_recipe(wl, s)
         sl = slice(s.offset, s.offset + s.length)
         if kind == "normal":
-            w[sl] = torch.randn(s.length, generator=g, device=device) * a
+            w[sl] = torch.randn(s.length, generator=g, device=w.device) * a
         elif kind == "uniform":
-            w[sl] = (torch.rand(s.length, generator=g, device=device) * 2 - 1) * a
+            w[sl] = (torch.rand(s.length, generator=g, device=w.device) * 2 - 1) * a
         else:
             w[sl] = a
-    return reps, w, v
+
+
+def device_weights(wl, seed, device):
+    """torch w, v on `device` drawn as device_inputs(wl, seed, ...) draws
+    them (same recipe and seed): extra weight/velocity sets for a benchmark
+    that rotates them independently of the replicas."""
+    import torch
+
+    g = torch.Generator(device=device)
+    w = torch.zeros(wl.padded, dtype=torch.float32, device=device)
+    v = torch.zeros(wl.padded, dtype=torch.float32, device=device)
+    _draw_weights(wl, seed + 1, g, w)
+    return w, v
 
 
 # ---------------------------------------------------------------- random tables for tests
