@@ -705,3 +705,21 @@ def test_balance_drains_the_plans_stream(fc):
     side.synchronize()
     assert same_bits(w_d.cpu().numpy(), w) == 0 and same_bits(v_d.cpu().numpy(), v) == 0
     p.close()
+
+
+def test_balance_with_full_lds_keeps_equal_shares(fc):
+    """Two blocks whose equal share of each round already fills all 160 LDS
+    slots (640 tiles, 2 rounds): no unequal division fits, so the shares
+    fc_plan_balance writes stay equal (160 and 160); the steps after it stay
+    bit-exact."""
+    n = 2 * 2 * 160 * 256
+    segs = [(0, n, 1.0, 1.0)]
+    p = fc.Plan(segs, 6, "f32", "tree", schedule=3, max_blocks=2)
+    info = p.info()
+    p.close()
+    assert (info.ntiles, info.rounds, info.lds_bytes) == (640, 2, 160 * 1024)
+    rates = []
+    bad = run_steps(fc, segs, 6, "f32", "tree", np.random.default_rng(21), steps=3, opts=dict(schedule=3, max_blocks=2),
+                    after_step=lambda plan: rates.append(plan.balance()))
+    assert bad == 0
+    assert sum(1 for r in rates[-1] if r > 0) == 2
