@@ -119,8 +119,9 @@ typedef enum {
 /* Launch shape.  Results are bit-identical for every allowed setting; the
  * fields only change speed.  Zero selects the default, which depends on the
  * schedule, the replica type, K and the plan's size (measured on MI355X):
- * RESIDENT -> (1 vector, 16 replicas, 64-lane tiles), where vecs_per_thread
- * and kchunk may also name (2, 4); otherwise fp32 in tree
+ * RESIDENT -> 64-lane tiles of (2 vectors, batches of 4 replicas) for fp32
+ * replicas with K <= 16, else (1 vector, batches of 16); vecs_per_thread and
+ * kchunk may name either; otherwise fp32 in tree
  * order with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8
  * waves (see k_waves); fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
  * 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads

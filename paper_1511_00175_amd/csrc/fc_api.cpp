@@ -365,10 +365,13 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess)
         return FC_EHIP;
     int res_u = 1, res_c = 16;  // the resident tiles' lane vectors and batch
+    fc::default_resident_shape(gdt, K, res_u, res_c);
     if (sched_req == FC_SCHED_RESIDENT && opts->vecs_per_thread) {
         res_u = opts->vecs_per_thread;
         res_c = opts->kchunk ? opts->kchunk : (res_u == 2 ? 4 : 16);
     } else if (sched_req == FC_SCHED_RESIDENT && opts->kchunk) {
+        // a batch alone names single-vector tiles, as validate_opts checks
+        res_u = 1;
         res_c = opts->kchunk;
     }
     const uint64_t tile_vecs_r = 64 * static_cast<uint64_t>(res_u);

@@ -58,6 +58,23 @@ inline int ksplit_span(int K, int w, int c) {
 // (lane vectors, replicas per batch) of the resident kernel's tiles; with
 // two vectors per lane K / kchunk must stay below 128 (stack depth 7).
 inline bool resident_pair(int u, int c) { return (u == 1 && c == 16) || (u == 2 && c == 4); }
+
+// Default resident tiles: fp32 replicas with K <= 16 take 2 lane-vectors and
+// batches of 4 (each wave reads 2 KiB of a replica per tile), the others 1
+// lane-vector and batches of 16.  Measured on MI355X with XCD-balanced
+// shares, us per step, (1, 16) vs (2, 4): VGG-19 K=16 1871-1884 vs
+// 1859-1862, 40 M x K=16 534.5 vs 512.0, 40 M x K=12 427.3 vs 417.0,
+// 20 M x K=8 164.1 vs 161.4, 2^20 x K=16 14.8 vs 14.1, 2^23 x K=16 98.8 vs
+// 99.3; for larger K the single vector with batches of 16 keeps more bytes
+// in flight per register (GoogLeNet K=128 540 vs 548, AlexNet fp16 K=128
+// 2611 vs 2705, NiN K=32 equal).
+inline void default_resident_shape(fc_dtype gdt, int K, int& u, int& c) {
+    if (gdt == FC_F32 && K <= 16) {
+        u = 2; c = 4;
+    } else {
+        u = 1; c = 16;
+    }
+}
 inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128; }
 
 inline bool compiled_pair(int u, int c) {

@@ -215,17 +215,30 @@ def test_schedule_resolution(fc):
                             (129, "f16", 2)):
         info = fc.Plan(small, K, dtype, "tree").info()
         assert (info.schedule, info.rounds) == (sched, 0), (K, dtype)
+    # a batch alone names single-vector resident tiles, also where the
+    # default would take two vectors (fp32, K <= 16)
+    info = fc.Plan(small, 8, "f32", "tree", schedule=3, kchunk=16).info()
+    assert (info.vecs_per_thread, info.kchunk) == (1, 16)
+    assert run_steps(fc, small, 8, "f32", "tree", np.random.default_rng(4), steps=2,
+                     opts=dict(schedule=3, kchunk=16)) == 0
     # 2^20 x K=4 fp32 (32 MiB of replicas + 16 MiB of w, v): fused; K=16 (80 MiB): resident
     assert fc.Plan([(0, 1 << 20, 1, 1)], 4, "f32", "tree").info().schedule == 1
     assert fc.Plan([(0, 1 << 20, 1, 1)], 16, "f32", "tree").info().schedule == 3
-    for K, dtype in ((1, "f32"), (64, "f32"), (1024, "f32"), (129, "f16")):
+    for K, dtype in ((1, "f32"), (16, "f32"), (17, "f32"), (64, "f32"), (1024, "f32"), (129, "f16")):
         info = fc.Plan(small, K, dtype, "tree", schedule=3).info()
         assert (info.schedule, info.scratch_bytes, info.rounds) == (3, 0, 1), (K, dtype)
-        assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
-        # 3 tiles of 256 elements and one of 232, then the 5-element segment's
-        # vector and its tail tile: one tile per block; LDS for the 6 tiles a
-        # block could be given (fc_plan_balance), 1 KiB each
-        assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 6 * 1024)
+        if dtype == "f32" and K <= 16:
+            # tiles of 2 vectors per lane, batches of 4: 2 tiles of 512 elements
+            # (the second of 488), then the 5-element segment's vector and its
+            # tail tile; LDS for the 4 tiles a block could be given, 2 KiB each
+            assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 2, 4, 1)
+            assert (info.ntiles, info.grid, info.lds_bytes) == (4, 4, 4 * 2048)
+        else:
+            assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
+            # 3 tiles of 256 elements and one of 232, then the 5-element segment's
+            # vector and its tail tile: one tile per block; LDS for the 6 tiles a
+            # block could be given (fc_plan_balance), 1 KiB each
+            assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 6 * 1024)
     # 160 tiles per block fill 160 KiB of LDS: 256-element tiles for cus * 160 tiles fit
     fits = [(0, cus * 160 * 256, 1, 1)]
     big = [(0, cus * 160 * 256 + 4, 1, 1)]
@@ -714,12 +727,13 @@ def test_balance_with_full_lds_keeps_equal_shares(fc):
     bit-exact."""
     n = 2 * 2 * 160 * 256
     segs = [(0, n, 1.0, 1.0)]
-    p = fc.Plan(segs, 6, "f32", "tree", schedule=3, max_blocks=2)
+    opts = dict(schedule=3, max_blocks=2, vecs_per_thread=1)
+    p = fc.Plan(segs, 6, "f32", "tree", **opts)
     info = p.info()
     p.close()
     assert (info.ntiles, info.rounds, info.lds_bytes) == (640, 2, 160 * 1024)
     rates = []
-    bad = run_steps(fc, segs, 6, "f32", "tree", np.random.default_rng(21), steps=3, opts=dict(schedule=3, max_blocks=2),
+    bad = run_steps(fc, segs, 6, "f32", "tree", np.random.default_rng(21), steps=3, opts=opts,
                     after_step=lambda plan: rates.append(plan.balance()))
     assert bad == 0
     assert sum(1 for r in rates[-1] if r > 0) == 2
