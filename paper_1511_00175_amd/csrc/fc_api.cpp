@@ -13,6 +13,7 @@
 
 #include "fc.h"
 #include "fc_internal.h"
+#include "fc_partition.h"
 #include "fc_shape.h"
 
 using fc::Tile;
@@ -151,33 +152,6 @@ hipError_t launch_resident(fc_plan* p, int mode, const fc::ReduceArgs& r, hipStr
 hipError_t clear_clock(fc_plan* p) {
     std::vector<unsigned long long> z(static_cast<size_t>(p->res_grid) * fc::RESIDENT_CLOCK_WORDS, 0ull);
     return hipMemcpy(p->d_clock, z.data(), z.size() * sizeof(unsigned long long), hipMemcpyHostToDevice);
-}
-
-// The resident ranges for per-block weights w (one per block of the grid):
-// in every round, block b's share of the round's tiles is proportional to
-// w[b].  Returns the most tiles any block gets.
-int resident_ranges(int ntiles, int rounds, int grid, const std::vector<double>& w, std::vector<int>& ranges) {
-    std::vector<double> cum(static_cast<size_t>(grid) + 1, 0.0);
-    for (int b = 0; b < grid; ++b) cum[b + 1] = cum[b] + w[b];
-    ranges.assign(static_cast<size_t>(grid) * rounds + 1, 0);
-    int most = 0;
-    for (int r = 0; r < rounds; ++r) {
-        const uint64_t lo = static_cast<uint64_t>(ntiles) * r / rounds;
-        const uint64_t hi = static_cast<uint64_t>(ntiles) * (r + 1) / rounds;
-        ranges[static_cast<size_t>(r) * grid] = static_cast<int>(lo);
-        for (int b = 1; b < grid; ++b) {
-            uint64_t x = lo + static_cast<uint64_t>(static_cast<double>(hi - lo) * (cum[b] / cum[grid]));
-            x = std::min(hi, std::max<uint64_t>(x, ranges[static_cast<size_t>(r) * grid + b - 1]));
-            ranges[static_cast<size_t>(r) * grid + b] = static_cast<int>(x);
-        }
-        const int end = static_cast<int>(hi);
-        ranges[static_cast<size_t>(r + 1) * grid] = end;  // the next round's first, or the end
-        for (int b = 0; b < grid; ++b) {
-            const size_t i = static_cast<size_t>(r) * grid + b;
-            most = std::max(most, (b + 1 < grid ? ranges[i + 1] : end) - ranges[i]);
-        }
-    }
-    return most;
 }
 
 void note_stream(fc_plan* p, hipStream_t s) {
@@ -489,9 +463,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
             delete p;
             return FC_ENOMEM;
         }
-        // range i = [i * ntiles / R, (i + 1) * ntiles / R): at most ceil(ntiles / R) tiles
-        for (uint64_t i = 0; i <= res_ranges; ++i)
-            ranges[i] = static_cast<int>(static_cast<uint64_t>(p->ntiles) * i / res_ranges);
+        fc::equal_ranges(p->ntiles, p->res_rounds, res_grid, ranges);
     }
 
     bool ok = hipMalloc(&p->d_tiles, std::max<size_t>(tiles.size(), 1) * sizeof(Tile)) == hipSuccess &&
@@ -572,12 +544,12 @@ int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
     const int G = p->res_grid, R = p->res_rounds;
     std::vector<unsigned long long> c;
     std::vector<int> xcd;
-    std::vector<double> w;
+    std::vector<double> rel_b;
     std::vector<int> ranges;
     try {
         c.resize(static_cast<size_t>(G) * fc::RESIDENT_CLOCK_WORDS);
         xcd.resize(static_cast<size_t>(G));
-        w.resize(static_cast<size_t>(G));
+        rel_b.resize(static_cast<size_t>(G));
     } catch (const std::bad_alloc&) {
         return FC_ENOMEM;
     }
@@ -604,21 +576,11 @@ int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
     for (int x = 0; x < NX; ++x) rel[x] = ticks[x] > 0.0 ? tiles[x] / ticks[x] / mean : 1.0;
     // shares proportional to the XCD's rate, drawn toward equal shares until
     // every block's tiles fit its LDS; equal shares always fit
-    bool fit = false;
-    for (double lam = 1.0; lam >= 1.0 / 64; lam *= 0.5) {
-        for (int b = 0; b < G; ++b) w[b] = 1.0 + lam * (rel[xcd[b]] - 1.0);
-        try {
-            if (static_cast<int64_t>(resident_ranges(p->ntiles, R, G, w, ranges)) * p->res_slot <= p->res_lds) {
-                fit = true;
-                break;
-            }
-        } catch (const std::bad_alloc&) {
-            return FC_ENOMEM;
-        }
-    }
-    if (!fit) {
-        const size_t n = static_cast<size_t>(G) * R;
-        for (size_t i = 0; i <= n; ++i) ranges[i] = static_cast<int>(static_cast<uint64_t>(p->ntiles) * i / n);
+    for (int b = 0; b < G; ++b) rel_b[b] = rel[xcd[b]];
+    try {
+        (void)fc::balanced_ranges(p->ntiles, R, G, rel_b, p->res_lds / p->res_slot, ranges);
+    } catch (const std::bad_alloc&) {
+        return FC_ENOMEM;
     }
     if (hipMemcpy(p->d_ranges, ranges.data(), ranges.size() * sizeof(int), hipMemcpyHostToDevice) != hipSuccess ||
         clear_clock(p) != hipSuccess)
