@@ -150,8 +150,12 @@ hipError_t launch_resident(fc_plan* p, int mode, const fc::ReduceArgs& r, hipStr
 
 // Zero the per-block record of the resident launches (synchronous).
 hipError_t clear_clock(fc_plan* p) {
-    std::vector<unsigned long long> z(static_cast<size_t>(p->res_grid) * fc::RESIDENT_CLOCK_WORDS, 0ull);
-    return hipMemcpy(p->d_clock, z.data(), z.size() * sizeof(unsigned long long), hipMemcpyHostToDevice);
+    try {
+        std::vector<unsigned long long> z(static_cast<size_t>(p->res_grid) * fc::RESIDENT_CLOCK_WORDS, 0ull);
+        return hipMemcpy(p->d_clock, z.data(), z.size() * sizeof(unsigned long long), hipMemcpyHostToDevice);
+    } catch (const std::bad_alloc&) {
+        return hipErrorOutOfMemory;  // no exception leaves the C ABI
+    }
 }
 
 void note_stream(fc_plan* p, hipStream_t s) {
