@@ -291,6 +291,20 @@ int launch(fc_plan* p, int kind, hipStream_t s, F&& go) {
     return rc;
 }
 
+// Every entry point returns a code: a host allocation that fails inside one
+// (validation spans, pointer-table copies, event bookkeeping) is FC_ENOMEM,
+// and no exception leaves the C ABI.
+template <typename F>
+int guarded(F&& body) {
+    try {
+        return body();
+    } catch (const std::bad_alloc&) {
+        return FC_ENOMEM;
+    } catch (...) {
+        return FC_EHIP;
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -535,7 +549,7 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     return FC_OK;
 }
 
-int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
+static int fc_plan_balance_body(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
     if (!p || n_rate < 0 || (n_rate > 0 && !xcd_rate)) return FC_EINVAL;
     for (int i = 0; i < n_rate; ++i) xcd_rate[i] = 0.0f;
     if (p->schedule != FC_SCHED_RESIDENT || !p->res_record) return FC_OK;
@@ -600,7 +614,7 @@ int fc_plan_set_timing(fc_plan* p, int enable) {
     return FC_OK;
 }
 
-int fc_plan_read_timing(fc_plan* p, fc_timing* t) {
+static int fc_plan_read_timing_body(fc_plan* p, fc_timing* t) {
     if (!p || !t) return FC_EINVAL;
     std::memset(t, 0, sizeof(*t));
     int rc = FC_OK;
@@ -650,7 +664,7 @@ int check_dsts(const fc_plan* p, float* const* dst, std::vector<Span>& spans) {
 
 }  // namespace
 
-int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* stream) {
+static int fc_tree_reduce_body(fc_plan* p, const void* const* grads, float* out, void* stream) {
     if (!p || !out) return FC_EINVAL;
     if (!aligned16(out)) return FC_EALIGN;
     std::vector<Span> spans;
@@ -679,7 +693,7 @@ int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* strea
     return rc;
 }
 
-int fc_sgd_step(fc_plan* p, float* w, float* v, const float* g, float lr, float mu, float wd, int batch,
+static int fc_sgd_step_body(fc_plan* p, float* w, float* v, const float* g, float lr, float mu, float wd, int batch,
                 void* stream) {
     if (!p || !w || !v || !g || batch < 1) return FC_EINVAL;
     if (!aligned16(w) || !aligned16(v) || !aligned16(g)) return FC_EALIGN;
@@ -705,7 +719,7 @@ int fc_sgd_step(fc_plan* p, float* w, float* v, const float* g, float lr, float 
     return rc;
 }
 
-int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) {
+static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, void* stream) {
     if (!p || !src || !dst) return FC_EINVAL;
     if (!aligned16(src)) return FC_EALIGN;
     std::vector<Span> spans = {span_of(p, src, 4, false, ID_SRC, false)};
@@ -728,7 +742,7 @@ int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) 
     return rc;
 }
 
-int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
+static int fc_step_body(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
             float* out, float* const* bcast_dst, void* stream) {
     if (!p || !w || !v || batch < 1) return FC_EINVAL;
     if (!aligned16(w) || !aligned16(v) || (out && !aligned16(out))) return FC_EALIGN;
@@ -856,6 +870,32 @@ int fc_train(fc_plan* p, const void* const* grads, float* w, float* v, const fc_
         if (rc) return rc;
     }
     return FC_OK;
+}
+
+int fc_plan_read_timing(fc_plan* p, fc_timing* t) {
+    return guarded([&] { return fc_plan_read_timing_body(p, t); });
+}
+
+int fc_tree_reduce(fc_plan* p, const void* const* grads, float* out, void* stream) {
+    return guarded([&] { return fc_tree_reduce_body(p, grads, out, stream); });
+}
+
+int fc_sgd_step(fc_plan* p, float* w, float* v, const float* g, float lr, float mu, float wd, int batch,
+                void* stream) {
+    return guarded([&] { return fc_sgd_step_body(p, w, v, g, lr, mu, wd, batch, stream); });
+}
+
+int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) {
+    return guarded([&] { return fc_broadcast_body(p, src, dst, stream); });
+}
+
+int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
+            float* out, float* const* bcast_dst, void* stream) {
+    return guarded([&] { return fc_step_body(p, grads, w, v, lr, mu, wd, batch, out, bcast_dst, stream); });
+}
+
+int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {
+    return guarded([&] { return fc_plan_balance_body(p, stream, xcd_rate, n_rate); });
 }
 
 }  // extern "C"
