@@ -442,10 +442,11 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
 
 // The end of the work on one lane-vector whose raw sum s[0..V-1] is known:
 // reduce-only, store the sum; step, update w and v and store w', v' (and the
-// raw sum and the broadcast copies when asked for).
-template <int V, int MODE>
+// raw sum and the broadcast copies when asked for).  KEEP: instead of storing
+// the broadcast copies, leave w' in keep[0..V-1] for the caller to store.
+template <int V, int MODE, bool KEEP = false>
 __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uint32_t off, const float* s,
-                                       float lr_j, float wd_j) {
+                                       float lr_j, float wd_j, float* keep = nullptr) {
     if constexpr (MODE == MODE_REDUCE) {
         st32r<V>(gwrite(a.out) + start4, off, s);
     } else {
@@ -457,8 +458,13 @@ __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uin
         st32r<V>(gwrite(a.w) + start4, off, wn);
         st32r<V>(gwrite(a.v) + start4, off, vn);
         if (a.out) st32r<V>(gwrite(a.out) + start4, off, s);
-        if (a.dst)
+        if constexpr (KEEP) {
+            if (a.dst)
+#pragma unroll
+                for (int i = 0; i < V; ++i) keep[i] = wn[i];
+        } else if (a.dst) {
             for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
+        }
     }
 }
 
@@ -640,16 +646,46 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
                 lr_j = a.lr * ldc(a.mults, 2 * sj);
                 wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
             }
-            const float* slot = slots + j * SLOT;
+            float* slot = slots + j * SLOT;
             const uint64_t start4 = tile.start * 4;
             if (!(tile.seg & TAIL_BIT)) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const uint32_t vi = lane + 64 * u;
-                    if (vi < tile.count) finish<4, MODE>(a, start4, vi * 16, slot + vi * 4, lr_j, wd_j);
+                    if (vi < tile.count)
+                        finish<4, MODE, true>(a, start4, vi * 16, slot + vi * 4, lr_j, wd_j, slot + vi * 4);
                 }
             } else if (lane < tile.count) {
-                finish<1, MODE>(a, start4, lane * 4, slot + lane, lr_j, wd_j);
+                finish<1, MODE, true>(a, start4, lane * 4, slot + lane, lr_j, wd_j, slot + lane);
+            }
+        }
+        if constexpr (MODE == MODE_STEP) {
+            if (a.dst) {
+                // Phase 3, the broadcast: w' now sits in the slots.  The block
+                // writes one destination at a time, its waves kept in step by
+                // a barrier per destination, so that each destination receives
+                // the block's whole range as one contiguous run (measured on
+                // MI355X: 3-4% faster than storing all K copies of a tile
+                // before the next tile).  Wave q stores the tiles it updated,
+                // so it reads back only slots it wrote itself.
+                for (int k = 0; k < a.K; ++k) {
+                    const gptr_w_t d = gwrite(ldc(a.dst, k));
+                    for (int j = q; j < hi - lo; j += W) {
+                        const Tile tile = ld_tile(a.tiles, lo + j);
+                        const float* slot = slots + j * SLOT;
+                        const uint64_t start4 = tile.start * 4;
+                        if (!(tile.seg & TAIL_BIT)) {
+#pragma unroll
+                            for (int u = 0; u < U; ++u) {
+                                const uint32_t vi = lane + 64 * u;
+                                if (vi < tile.count) st32r<4>(d + start4, vi * 16, slot + vi * 4);
+                            }
+                        } else if (lane < tile.count) {
+                            st32r<1>(d + start4, lane * 4, slot + lane);
+                        }
+                    }
+                    __syncthreads();
+                }
             }
         }
         __syncthreads();  // the next round's phase 1 overwrites the slots

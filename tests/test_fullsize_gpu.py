@@ -9,8 +9,9 @@ device, three fused steps run on the GPU (fc_plan_balance after the first),
 and at every segment's first, second, last and one random element plus 1500
 random elements the oracle recomputes the same three steps from the gathered
 inputs; w' and v' must match bit for bit.
-A property that holds at any size is checked on the whole buffer: the fused
-step equals reduce, then SGD, then (for GoogLeNet) nothing else differs.
+Properties that hold at any size are checked on the whole buffer: the fused
+step equals reduce, then SGD (GoogLeNet), and the broadcast copies and raw
+sum fused into the step equal w' and the reduce's sum (GoogLeNet, VGG-19).
 """
 import numpy as np
 import pytest
@@ -97,6 +98,44 @@ def test_fullsize_fused_equals_composed(fc):
     assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
     assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
     plan.close()
+
+
+@pytest.mark.parametrize("name", ["googlenet", "vgg19"])
+def test_fullsize_broadcast(fc, name):
+    """The raw sum and the broadcast of w' fused into the step at full size
+    (GoogLeNet: K = 128 copies, one resident round; VGG-19: K = 16 copies,
+    14 rounds), shares rebalanced per XCD after it: every worker copy equals
+    w' bit for bit on every parameter and keeps its fill value on the
+    padding, the raw sum equals fc_tree_reduce's, and w', v' equal those of
+    a step without either (properties that hold at any size)."""
+    import torch
+    wl = tables.get(name)
+    dev = torch.device("cuda:0")
+    reps, w, v = gen.device_inputs(wl, 5, dev)
+    w2, v2 = w.clone(), v.clone()
+    n = w.numel()
+    mask = torch.zeros(n, dtype=torch.bool, device=dev)
+    for s in wl.segments:
+        mask[s.offset:s.offset + s.length] = True
+    dst = torch.full((wl.K, n), -2.0, device=dev)
+    out = torch.full((n,), -1.0, device=dev)
+    g = torch.full((n,), -1.0, device=dev)
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
+    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=dst)
+    plan.balance()
+    plan.step(reps, w2, v2, wl.lr, wl.mu, wl.wd, wl.batch)
+    plan.tree_reduce(reps, g)
+    torch.cuda.synchronize()
+    plan.close()
+    assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
+    assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
+    assert torch.equal(out.view(torch.int32), g.view(torch.int32))
+    wm = w[mask].view(torch.int32)
+    for k in range(wl.K):
+        assert torch.equal(dst[k][mask].view(torch.int32), wm), k
+        assert bool((dst[k][~mask] == -2.0).all()), k
+    del reps, w, v, w2, v2, dst, out, g
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("dtype,schedule", [("f16", 1), ("f16", 3), ("f32", 2), ("f32", 3)])

@@ -462,14 +462,15 @@ def test_resident_matches_oracle(fc, K, max_blocks, vecs, dtype, order):
     """The resident schedule (phase 1: reduce each block's tiles into LDS;
     phase 2: finish them from LDS), with tiles of 64 lanes x 1 vector
     (batches of 16) or x 2 vectors (batches of 4): reduce and steps with raw
-    sum and broadcast, blocks with one tile or with many, both orders."""
+    sum and broadcast (phase 3: one destination at a time, over one round or
+    many), blocks with one tile or with many, both orders."""
     segs = table(14000 + K, dtype, nseg=5, max_len=3000 if K < 500 else 800)
     rng = np.random.default_rng(K + 3)
     opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     bad, _, _ = run_reduce(fc, segs, K, dtype, order, rng, opts=opts)
     assert bad == 0
     assert run_steps(fc, segs, K, dtype, order, rng, steps=2, opts=opts, with_out=True,
-                     with_bcast=K <= 17) == 0
+                     with_bcast=K <= 64) == 0
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
