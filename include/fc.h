@@ -186,9 +186,14 @@ int fc_sgd_step(fc_plan* plan, float* w, float* v, const float* g, float lr, flo
                 int batch, void* stream);
 
 /* Send one fp32 vector back down the tree (Fig. 3 caption): dst[k][i] =
- * src[i] for every worker k < K and segment element i.
+ * src[i] for every worker k < K and segment element i; other elements of the
+ * destinations are not written.
  *   dst : host array of K device pointers.  No destination may overlap src
- *         or another destination (FC_EALIAS). */
+ *         or another destination (FC_EALIAS).
+ * On a plan with the resident schedule it runs the plan's rounds of one
+ * persistent block per compute unit (each block stages its range of src in
+ * LDS and stores it one destination at a time); otherwise one block per
+ * tile. */
 int fc_broadcast(fc_plan* plan, const float* src, float* const* dst, void* stream);
 
 /* The whole step in one pass over memory: reduce, average, SGD, write back,

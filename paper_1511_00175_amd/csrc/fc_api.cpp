@@ -501,7 +501,8 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
             // compute unit's whole LDS, so that no plan lowers another's limit
             const size_t lds = static_cast<size_t>(lds_cu);
             ok = (gdt == FC_F16 ? fc::prepare_resident_f16(sh, lds) : fc::prepare_resident_f32(sh, lds)) ==
-                 hipSuccess;
+                     hipSuccess &&
+                 fc::prepare_resident_bcast(sh, lds) == hipSuccess;
         }
     }
     if (ok && !tiles.empty())
@@ -737,7 +738,17 @@ static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, vo
     a.src = src;
     a.dst = p->d_dst;
     a.K = p->K;
-    rc = launch(p, FC_KERNEL_BCAST, s, [&] { return fc::launch_bcast(p->shape, p->grid, a, s); });
+    rc = launch(p, FC_KERNEL_BCAST, s, [&] {
+        if (p->schedule != FC_SCHED_RESIDENT) return fc::launch_bcast(p->shape, p->grid, a, s);
+        // resident plans: the step's ranges, one launch per round
+        for (int round = 0; round < p->res_rounds; ++round) {
+            a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
+            const hipError_t e =
+                fc::launch_resident_bcast(p->shape, p->res_grid, static_cast<size_t>(p->res_lds), a, s);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    });
     note_stream(p, s);
     return rc;
 }

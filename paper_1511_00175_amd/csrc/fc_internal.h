@@ -90,6 +90,7 @@ struct BcastArgs {
     const float* src;
     float* const* dst;
     int K;
+    const int* ranges;            // resident plans: gridDim.x + 1 tile indices of one round
 };
 
 // Largest pending-subtree stack depth compiled (stack depths 5, 7 and 10 are
@@ -106,6 +107,8 @@ hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceAr
 hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s);
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s);
+hipError_t launch_resident_bcast(const Shape& sh, int grid, size_t lds, const BcastArgs& a, hipStream_t s);
+hipError_t prepare_resident_bcast(const Shape& sh, size_t lds);
 hipError_t prepare_resident_f32(const Shape& sh, size_t lds);
 hipError_t prepare_resident_f16(const Shape& sh, size_t lds);
 hipError_t launch_resident_f32(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a, hipStream_t s);

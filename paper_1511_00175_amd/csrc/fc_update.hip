@@ -1,5 +1,6 @@
 // SGD-from-a-raw-sum and broadcast kernels: one block per tile, one thread
-// per lane of the tile.
+// per lane of the tile; on resident plans the broadcast runs one persistent
+// block per CU.
 #include "fc_device.h"
 
 namespace fc {
@@ -20,6 +21,31 @@ hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream
     };
     if (sh.vecs == 4) return go(I<4>{});
     return pick<1, 2>(sh.vecs, go);
+}
+
+// The resident broadcast for a plan's resident tile shape (1 or 2 lane
+// vectors); `lds` is the plan's LDS per block.
+template <class F> hipError_t pick_resident_bcast(const Shape& sh, F&& f) {
+    if (sh.block != 64) return hipErrorInvalidValue;
+    if (sh.vecs == 1) return f(&resident_bcast_kernel<RESIDENT_WAVES, 1>);
+    if (sh.vecs == 2) return f(&resident_bcast_kernel<RESIDENT_WAVES, 2>);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_resident_bcast(const Shape& sh, int grid, size_t lds, const BcastArgs& a, hipStream_t s) {
+    return pick_resident_bcast(sh, [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(grid), dim3(64 * RESIDENT_WAVES), lds, s, a);
+        return hipGetLastError();
+    });
+}
+
+// Allow up to `lds` bytes of dynamic LDS for the kernel (a property of the
+// kernel, set when a resident plan is created, like the step kernels').
+hipError_t prepare_resident_bcast(const Shape& sh, size_t lds) {
+    return pick_resident_bcast(sh, [&](auto kernel) {
+        return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   static_cast<int>(lds));
+    });
 }
 
 // Read probe: a plain streaming read of one contiguous buffer, the ceiling a

@@ -316,6 +316,37 @@ def test_fused_equals_composed(fc):
         assert same_bits(a.cpu().numpy(), b.cpu().numpy()) == 0
 
 
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("schedule,max_blocks,vecs", [(0, 0, 0), (1, 0, 0), (2, 0, 0), (3, 0, 1), (3, 0, 2),
+                                                      (3, 1, 1), (3, 1, 2), (3, 2, 1)])
+@pytest.mark.parametrize("K", [1, 5, 40])
+def test_broadcast_matches_oracle(fc, K, schedule, max_blocks, vecs, dtype):
+    """fc_broadcast on each schedule's tile map: on resident plans one
+    persistent block per CU stages its range of the source in LDS and stores
+    it one destination at a time (one round, or many with few blocks); on the
+    others one block per tile.  Every destination gets the source's bits on
+    every segment element (special values included) and keeps its fill
+    value elsewhere; the replica type only changes the plan's tile map."""
+    import torch
+    segs = table(15000 + K, dtype, nseg=8, max_len=30000)  # 124-177 K elements: 485+ tiles of 256
+    n = alloc_len(segs)
+    rng = np.random.default_rng(K * 31 + schedule * 7 + max_blocks)
+    src = host_replicas(rng, 1, n, np.float32, special=True)[0]
+    expect = oracle.broadcast(segs, src, [np.full(n, -2.0, np.float32) for _ in range(K)])
+    opts = dict(schedule=schedule, max_blocks=max_blocks) if schedule else {}
+    if vecs:
+        opts["vecs_per_thread"] = vecs
+    plan = fc.Plan(segs, K, dtype, "tree", **opts)
+    if schedule == 3 and max_blocks:
+        assert plan.info().rounds > 1
+    dst = torch.full((K, n), -2.0, device="cuda")
+    plan.broadcast(to_dev(src), dst)
+    torch.cuda.synchronize()
+    got = dst.cpu().numpy()
+    plan.close()
+    assert sum(same_bits(got[k], expect[k]) for k in range(K)) == 0
+
+
 def test_repeatable(fc):
     """The same inputs give the same bits on every run (FAQ 6: no
     nondeterministic techniques)."""
