@@ -55,6 +55,7 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 
 template <int N> constexpr int ilog2() { return N <= 1 ? 0 : 1 + ilog2<N / 2>(); }
@@ -127,6 +128,37 @@ template <> struct Rep<FC_F32, 1> {
     }
     __device__ static __forceinline__ void widen(const raw& r, float* x) { x[0] = r; }
 };
+
+// fp32 replicas in the resident kernel: a lane's 4 values are two pairs of
+// consecutive elements, each read with its own 8-byte load, so that each load
+// instruction of a wave reads 512 contiguous bytes.  Measured on MI355X: a
+// plain stream of 8-byte lane loads is 1.3-1.6% faster than one of 16-byte
+// loads with the same bytes in flight, and the resident step with pairs
+// 2.7% faster on NiN K=32, 0.5% on GoogLeNet K=128 and VGG-19 K=16.  The
+// values stay 8-byte vectors until they are widened, so that each pair stays
+// one load.  OffPair holds the two pairs' byte offsets in the tile.
+constexpr int FC_F32_PAIRS = 2;
+struct OffPair {
+    uint32_t a, b;
+};
+template <> struct Rep<FC_F32_PAIRS, 4> {
+    struct raw {
+        u2 lo, hi;
+    };
+    __device__ static __forceinline__ raw load(gptr_t base, const OffPair& o) {
+        raw r;
+        r.lo = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), o.a, 0,
+                                                                          CPOL_STREAM_LOAD));
+        r.hi = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), o.b, 0,
+                                                                          CPOL_STREAM_LOAD));
+        return r;
+    }
+    __device__ static __forceinline__ void widen(const raw& r, float* x) {
+        const f2 a = __builtin_bit_cast(f2, r.lo), b = __builtin_bit_cast(f2, r.hi);
+        x[0] = a.x; x[1] = a.y; x[2] = b.x; x[3] = b.y;
+    }
+};
+template <> struct Rep<FC_F32_PAIRS, 1> : Rep<FC_F32, 1> {};
 
 // fp16 storage: binary16 -> binary32 is exact for every pattern.  A lane
 // takes 4 consecutive fp16 values (8 bytes), so that the lane's fp32 weights,
@@ -221,9 +253,9 @@ template <int U, int V> __device__ __forceinline__ void add_right(Acc<U, V>& d, 
 
 // Replica k's vectors of this lane: the replica pointer comes from the plan's
 // table (scalar load), the tile start is added in scalar registers.
-template <int DT, int V, int U>
+template <int DT, int V, int U, typename O>
 __device__ __forceinline__ void load_leaf(const void* const* grads, int k, uint64_t start_bytes,
-                                          const uint32_t (&off)[U], typename Rep<DT, V>::raw (&r)[U]) {
+                                          const O (&off)[U], typename Rep<DT, V>::raw (&r)[U]) {
     const gptr_t base = gread(ldc(grads, k)) + start_bytes;
 #pragma unroll
     for (int u = 0; u < U; ++u) r[u] = Rep<DT, V>::load(base, off[u]);
@@ -278,9 +310,9 @@ __device__ __forceinline__ void fold(const Acc<U, V> (&st)[D], int n, Acc<U, V>&
 }
 
 // Sum over the K replicas of V elements at e[u], u < U, in tree or linear order.
-template <int DT, int V, int U, int C, int MAXD, bool TREE>
+template <int DT, int V, int U, int C, int MAXD, bool TREE, typename O>
 __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t start_bytes,
-                                       const uint32_t (&off)[U], Acc<U, V>& acc) {
+                                       const O (&off)[U], Acc<U, V>& acc) {
     typedef typename Rep<DT, V>::raw raw_t;
     const int nfull = K / C;  // whole chunks of C consecutive replicas
     const int r = K - nfull * C;
@@ -291,7 +323,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
         for (int c = 0; c < nfull; ++c) {
             raw_t raw[C][U];
 #pragma unroll
-            for (int j = 0; j < C; ++j) load_leaf<DT, V, U>(grads, c * C + j, start_bytes, off, raw[j]);
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, O>(grads, c * C + j, start_bytes, off, raw[j]);
             Acc<U, V> x[C];
 #pragma unroll
             for (int j = 0; j < C; ++j) widen_leaf<DT, V, U>(x[j], raw[j]);
@@ -311,7 +343,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
             raw_t raw[C - 1][U];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i)
-                if (i < r) load_leaf<DT, V, U>(grads, nfull * C + i, start_bytes, off, raw[i]);
+                if (i < r) load_leaf<DT, V, U, O>(grads, nfull * C + i, start_bytes, off, raw[i]);
             Acc<U, V> rs[LC];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i) {
@@ -329,7 +361,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
         for (int c = 0; c < nfull; ++c) {
             raw_t raw[C][U];
 #pragma unroll
-            for (int j = 0; j < C; ++j) load_leaf<DT, V, U>(grads, c * C + j, start_bytes, off, raw[j]);
+            for (int j = 0; j < C; ++j) load_leaf<DT, V, U, O>(grads, c * C + j, start_bytes, off, raw[j]);
 #pragma unroll
             for (int j = 0; j < C; ++j) {
                 Acc<U, V> x;
@@ -343,7 +375,7 @@ __device__ __forceinline__ void reduce(const void* const* grads, int K, uint64_t
             raw_t raw[C - 1][U];
 #pragma unroll
             for (int i = 0; i < C - 1; ++i)
-                if (i < r) load_leaf<DT, V, U>(grads, nfull * C + i, start_bytes, off, raw[i]);
+                if (i < r) load_leaf<DT, V, U, O>(grads, nfull * C + i, start_bytes, off, raw[i]);
 #pragma unroll
             for (int i = 0; i < C - 1; ++i) {
                 if (i < r) {
@@ -640,19 +672,43 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
             const Tile tile = ld_tile(a.tiles, t);
             float* slot = slots + (t - lo) * SLOT;
             if (!(tile.seg & TAIL_BIT)) {
-                // vector u of the lane is tile vector lane + 64 u; idle lanes re-read vector 0
-                uint32_t off[U];
+                if constexpr (DT == FC_F32_PAIRS) {
+                    // the lane's values of the tile's elements [256 u, 256 u + 256): the
+                    // pairs at 256 u + 2 lane and 256 u + 128 + 2 lane; a pair past the
+                    // tile's elements re-reads pair 0
+                    const uint32_t ne = tile.count * 4;
+                    OffPair off[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const uint32_t vi = lane + 64 * u;
-                    off[u] = (vi < tile.count ? vi : 0u) * 4 * SG;
+                    for (int u = 0; u < U; ++u) {
+                        const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                        off[u].a = (e0 < ne ? e0 : 0u) * 4;
+                        off[u].b = (e1 < ne ? e1 : 0u) * 4;
+                    }
+                    Acc<U, 4> x;
+                    reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * 4, off, x);
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                        slot[e0] = x.a[u][0];
+                        slot[e0 + 1] = x.a[u][1];
+                        slot[e1] = x.a[u][2];
+                        slot[e1 + 1] = x.a[u][3];
+                    }
+                } else {
+                    // vector u of the lane is tile vector lane + 64 u; idle lanes re-read vector 0
+                    uint32_t off[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const uint32_t vi = lane + 64 * u;
+                        off[u] = (vi < tile.count ? vi : 0u) * 4 * SG;
+                    }
+                    Acc<U, 4> x;
+                    reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) slot[(lane + 64 * u) * 4 + i] = x.a[u][i];
                 }
-                Acc<U, 4> x;
-                reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) slot[(lane + 64 * u) * 4 + i] = x.a[u][i];
             } else {
                 const uint32_t vi = lane < tile.count ? lane : 0u;
                 const uint32_t off[1] = {vi * SG};
