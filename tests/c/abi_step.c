@@ -1,9 +1,10 @@
 /* A plain C client of the library's ABI (include/fc.h), with no Python and
  * no torch: it allocates device buffers with the HIP runtime's C API, runs
- * one fc_step, fc_plan_balance and one fc_tree_reduce per schedule on a small
- * ragged segment table, and compares every element bit for bit with the oracle's C
- * functions (the oracle is linked as test infrastructure) on the same
- * inputs.  Exit status 0 when everything matches; each failure is printed. */
+ * one fc_step, fc_plan_balance, fc_tree_reduce, fc_sgd_step on that sum and
+ * fc_broadcast of w' per schedule on a small ragged segment table, and
+ * compares every element bit for bit with the oracle's C functions (the
+ * oracle is linked as test infrastructure) on the same inputs.  Exit status
+ * 0 when everything matches; each failure is printed. */
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -21,6 +22,7 @@ int orc_tree_reduce(const orc_segment* segs, int nseg, int K, int dtype, int ord
                     float* out);
 int orc_step(const orc_segment* segs, int nseg, int K, int dtype, int order, const void* const* grads, float* w,
              float* v, float lr, float mu, float wd, int batch, float* scratch, float* out, float* const* bcast_dst);
+int orc_broadcast(const orc_segment* segs, int nseg, int K, const float* src, float* const* dst);
 
 enum { K = 37, NSEG = 3, N = 5248 };
 
@@ -66,8 +68,12 @@ int main(void) {
     float* out = malloc(sizeof(float) * N);
     float* scratch = malloc(sizeof(float) * N);
     float* got = malloc(sizeof(float) * N);
+    float* fill = malloc(sizeof(float) * N);
+    float* bc = malloc(sizeof(float) * K * N);
     const void* host_rows[K];
-    if (!reps || !w0 || !v0 || !w || !v || !out || !scratch || !got) return 2;
+    float* bc_rows[K];
+    if (!reps || !w0 || !v0 || !w || !v || !out || !scratch || !got || !fill || !bc) return 2;
+    for (int i = 0; i < N; ++i) fill[i] = -2.0f;  /* what the broadcast must leave outside the segments */
     for (int i = 0; i < K * N; ++i) reps[i] = draw(0.01f);
     for (int i = 0; i < N; ++i) {
         w0[i] = draw(0.1f);
@@ -75,11 +81,19 @@ int main(void) {
     }
     for (int k = 0; k < K; ++k) host_rows[k] = reps + (size_t)k * N;
 
-    float *d_reps, *d_w, *d_v, *d_out;
+    float *d_reps, *d_w, *d_v, *d_out, *d_w2, *d_v2, *d_bc;
     HIP_OK(hipMalloc((void**)&d_reps, sizeof(float) * K * N));
     HIP_OK(hipMalloc((void**)&d_w, sizeof(float) * N));
     HIP_OK(hipMalloc((void**)&d_v, sizeof(float) * N));
     HIP_OK(hipMalloc((void**)&d_out, sizeof(float) * N));
+    HIP_OK(hipMalloc((void**)&d_w2, sizeof(float) * N));
+    HIP_OK(hipMalloc((void**)&d_v2, sizeof(float) * N));
+    HIP_OK(hipMalloc((void**)&d_bc, sizeof(float) * K * N));
+    float* dev_bc[K];
+    for (int k = 0; k < K; ++k) {
+        dev_bc[k] = d_bc + (size_t)k * N;
+        bc_rows[k] = bc + (size_t)k * N;
+    }
     HIP_OK(hipMemcpy(d_reps, reps, sizeof(float) * K * N, hipMemcpyHostToDevice));
     const void* dev_rows[K];
     for (int k = 0; k < K; ++k) dev_rows[k] = d_reps + (size_t)k * N;
@@ -113,6 +127,12 @@ int main(void) {
         float rates[16];
         if (rc == FC_OK) rc = fc_plan_balance(plan, NULL, rates, 16);
         if (rc == FC_OK) rc = fc_tree_reduce(plan, dev_rows, d_out, NULL);
+        /* the composed path: SGD from that raw sum, then w' to K copies */
+        HIP_OK(hipMemcpy(d_w2, w0, sizeof(float) * N, hipMemcpyHostToDevice));
+        HIP_OK(hipMemcpy(d_v2, v0, sizeof(float) * N, hipMemcpyHostToDevice));
+        for (int k = 0; k < K; ++k) HIP_OK(hipMemcpy(dev_bc[k], fill, sizeof(float) * N, hipMemcpyHostToDevice));
+        if (rc == FC_OK) rc = fc_sgd_step(plan, d_w2, d_v2, d_out, lr, mu, wd, batch, NULL);
+        if (rc == FC_OK) rc = fc_broadcast(plan, d_w2, dev_bc, NULL);
         if (rc != FC_OK) {
             fprintf(stderr, "c client: schedule %d: %s\n", schedules[si], fc_strerror(rc));
             return 1;
@@ -132,13 +152,28 @@ int main(void) {
         for (int j = 0; j < NSEG; ++j)  /* only segment elements are defined in d_out */
             failed |= compare("raw sum", schedules[si], got + segs[j].offset, out + segs[j].offset,
                               (size_t)segs[j].length);
+        HIP_OK(hipMemcpy(got, d_w2, sizeof(float) * N, hipMemcpyDeviceToHost));
+        failed |= compare("w' (composed)", schedules[si], got, w, N);
+        HIP_OK(hipMemcpy(got, d_v2, sizeof(float) * N, hipMemcpyDeviceToHost));
+        failed |= compare("v' (composed)", schedules[si], got, v, N);
+        for (int k = 0; k < K; ++k) memcpy(bc_rows[k], fill, sizeof(float) * N);
+        if (orc_broadcast(osegs, NSEG, K, w, bc_rows) != 0) return 2;
+        for (int k = 0; k < K; ++k) {
+            HIP_OK(hipMemcpy(got, dev_bc[k], sizeof(float) * N, hipMemcpyDeviceToHost));
+            failed |= compare("broadcast copy", schedules[si], got, bc_rows[k], N);
+        }
         fc_plan_destroy(plan);
     }
     hipFree(d_reps);
     hipFree(d_w);
     hipFree(d_v);
     hipFree(d_out);
-    free(reps), free(w0), free(v0), free(w), free(v), free(out), free(scratch), free(got);
-    if (!failed) printf("c client: fc_step and fc_tree_reduce bit-exact vs the oracle (K=%d, %d segments, 4 schedules)\n", K, NSEG);
+    hipFree(d_w2);
+    hipFree(d_v2);
+    hipFree(d_bc);
+    free(reps), free(w0), free(v0), free(w), free(v), free(out), free(scratch), free(got), free(fill), free(bc);
+    if (!failed)
+        printf("c client: fc_step, fc_tree_reduce, fc_sgd_step and fc_broadcast bit-exact vs the oracle "
+               "(K=%d, %d segments, 4 schedules)\n", K, NSEG);
     return failed;
 }

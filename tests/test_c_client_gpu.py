@@ -1,7 +1,8 @@
 """The library used from plain C (tests/c/abi_step.c, built by
 __graft_entry__.build()): plan creation and error codes, fc_step and
 fc_tree_reduce in every schedule on device buffers from the HIP runtime's C
-API, compared bit for bit with the oracle's C functions."""
+API, then fc_sgd_step on that sum and fc_broadcast of w' (the composed
+path), compared bit for bit with the oracle's C functions."""
 import os
 import subprocess
 
