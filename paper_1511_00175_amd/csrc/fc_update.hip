@@ -49,28 +49,33 @@ hipError_t prepare_resident_bcast(const Shape& sh, size_t lds) {
 }
 
 // Read probe: a plain streaming read of one contiguous buffer, the ceiling a
-// read-bound kernel can reach.  Each lane sums 4 vectors of 16 bytes (nt
-// loads); the wave and then the block add their lanes' sums and lane 0 of the
-// block stores one float, which keeps the loads live.  The value's rounding
-// order is not specified: it is a bandwidth probe, not a result.
+// read-bound kernel can reach.  One block of 256 lanes per 16 KiB; each lane
+// sums 8 pieces of 8 bytes (nt loads: measured on MI355X, the fastest plain
+// read pattern found, ahead of 16-byte lanes or more bytes per lane); the
+// wave and then the block add their lanes' sums and lane 0 of the block
+// stores one float, which keeps the loads live.  The value's rounding order
+// is not specified: it is a bandwidth probe, not a result.
 constexpr int PROBE_THREADS = 256;
-constexpr int PROBE_VECS = 4;
+constexpr int PROBE_LOADS = 8;  // 8-byte loads per lane
 
-__global__ __launch_bounds__(PROBE_THREADS) void read_probe_kernel(const void* src, uint64_t nvec, float* out) {
-    const uint64_t first = static_cast<uint64_t>(blockIdx.x) * PROBE_THREADS * PROBE_VECS;
-    const gptr_t base = gread(src) + first * 16;
-    f4 v[PROBE_VECS];
+__global__ __launch_bounds__(PROBE_THREADS) void read_probe_kernel(const void* src, uint64_t n8, float* out) {
+    const uint64_t first = static_cast<uint64_t>(blockIdx.x) * PROBE_THREADS * PROBE_LOADS;
+    const gptr_t base = gread(src) + first * 8;
+    u2 v[PROBE_LOADS];
 #pragma unroll
-    for (int u = 0; u < PROBE_VECS; ++u) {
-        const uint64_t vi = first + threadIdx.x + u * PROBE_THREADS;
-        const uint32_t off = vi < nvec ? (threadIdx.x + u * PROBE_THREADS) * 16u : 0u;
-        v[u] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(rsrc((const void*)base), off, 0,
-                                                                           CPOL_STREAM_LOAD));
-        if (vi >= nvec) v[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int u = 0; u < PROBE_LOADS; ++u) {
+        const uint64_t i = first + threadIdx.x + u * PROBE_THREADS;
+        const uint32_t off = i < n8 ? (threadIdx.x + u * PROBE_THREADS) * 8u : 0u;
+        v[u] = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), off, 0,
+                                                                          CPOL_STREAM_LOAD));
+        if (i >= n8) v[u] = u2{0u, 0u};
     }
     float x = 0.0f;
 #pragma unroll
-    for (int u = 0; u < PROBE_VECS; ++u) x = x + ((v[u].x + v[u].y) + (v[u].z + v[u].w));
+    for (int u = 0; u < PROBE_LOADS; ++u) {
+        const f2 f = __builtin_bit_cast(f2, v[u]);
+        x = x + (f.x + f.y);
+    }
 #pragma unroll
     for (int d = 32; d >= 1; d /= 2) x = x + __shfl_xor(x, d, 64);
     __shared__ float wsum[PROBE_THREADS / 64];
@@ -85,14 +90,14 @@ __global__ __launch_bounds__(PROBE_THREADS) void read_probe_kernel(const void* s
 }
 
 uint64_t read_probe_blocks(uint64_t bytes) {
-    const uint64_t per = static_cast<uint64_t>(PROBE_THREADS) * PROBE_VECS * 16;
+    const uint64_t per = static_cast<uint64_t>(PROBE_THREADS) * PROBE_LOADS * 8;
     return (bytes + per - 1) / per;
 }
 
 hipError_t launch_read_probe(const void* src, uint64_t bytes, float* out, hipStream_t s) {
     const uint64_t blocks = read_probe_blocks(bytes);
     hipLaunchKernelGGL(read_probe_kernel, dim3(static_cast<unsigned>(blocks)), dim3(PROBE_THREADS), 0, s, src,
-                       bytes / 16, out);
+                       bytes / 8, out);
     return hipGetLastError();
 }
 
