@@ -106,7 +106,7 @@ typedef struct fc_plan fc_plan;
  *   with batches of 4 (vecs_per_thread 2, K < 512); no K split.
  * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
  *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
- *   round holds the plan or a parameter's replicas take at least 64 bytes
+ *   round holds the plan or a parameter's replicas take at least 48 bytes
  *   (K * bytes per element), else FUSED.  With a launch-shape field: TWO_PASS when they take more than
  *   256 bytes, else FUSED. */
 typedef enum {

@@ -84,13 +84,18 @@ inline bool compiled_pair(int u, int c) {
 
 // The resident schedule (sums parked in LDS, one persistent grid, one launch
 // per round) when one round of the grid holds the whole plan, or when a
-// parameter's replicas take at least 64 bytes.  Measured on MI355X (us per
+// parameter's replicas take at least 48 bytes.  Measured on MI355X (us per
 // step, resident vs the best other schedule): GoogLeNet K=128 543 vs 574,
 // NiN K=32 162 vs 175, VGG-19 K=16 1926 vs 1979 and K=32 3323 vs 3567 (14
 // rounds), AlexNet fp16 K=32/64/128 814/1379/2574 vs 890/1535/2579 and fp32
-// K=32/64 1431/2553 vs 1473/2810 (6 rounds); below 64 bytes the fused kernel
-// wins (VGG-19 K=8 1213 vs 1203, K=4 846 vs 766; AlexNet fp16 K=16 521 vs
-// 517), its update writes being a larger share of the bytes.
+// K=32/64 1431/2553 vs 1473/2810 (6 rounds).  With w and v kept out of the
+// Infinity Cache, at 48 bytes (fp32 K=12, fp16 K=24) resident wins at every
+// size tried: 143.7 M fp32 1510 vs 1634, 61 M 661 vs 673, 20 M 214 vs 227,
+// 2^25 366-384 vs 374-377; fp16 61 M 675 vs 711, 2^25 373 vs 383, 20 M 217
+// vs 235.  At 40 bytes the two trade places by size (within 5%), and at 32
+// bytes and below the fused kernel wins or ties (fp32 K=8: 61 M 492 vs 515,
+// 2^25 275 vs 293-303, 20 M 165 vs 165; fp16 K=16: 2^25 282 vs 292; VGG-19
+// K=4 766 vs 846), its update writes being a larger share of the bytes.
 // Steps of less than RESIDENT_MIN_BYTES of algorithmic traffic (a few
 // microseconds of HBM time) stay on the single-pass fused kernel, whose one
 // round trip to memory beats the resident kernel's two phases: measured on
@@ -102,7 +107,7 @@ inline bool compiled_pair(int u, int c) {
 constexpr uint64_t RESIDENT_MIN_BYTES = uint64_t(64) << 20;
 inline bool default_resident(int K, int bytes_per_element, int64_t rounds, uint64_t step_bytes) {
     if (step_bytes < RESIDENT_MIN_BYTES) return false;
-    return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 64;
+    return rounds == 1 || static_cast<int64_t>(K) * bytes_per_element >= 48;
 }
 
 // Resident launches record each block's rate (for fc_plan_balance) when a

@@ -251,8 +251,8 @@ def test_schedule_resolution(fc):
         assert info.scratch_bytes == (4 * big[0][1] if two else 0)
         p.close()
     # without a launch shape, plans of several rounds are resident when a
-    # parameter's replicas take at least 64 bytes
-    for K, dtype, sched in ((15, "f32", 1), (16, "f32", 3), (31, "f16", 1), (32, "f16", 3), (130, "f32", 3)):
+    # parameter's replicas take at least 48 bytes
+    for K, dtype, sched in ((11, "f32", 1), (12, "f32", 3), (23, "f16", 1), (24, "f16", 3), (130, "f32", 3)):
         p = fc.Plan(big, K, dtype, "tree")
         assert p.info().schedule == sched, (K, dtype)
         p.close()
