@@ -500,6 +500,9 @@ def test_resident_matches_oracle(fc, K, max_blocks, vecs, dtype, order):
     opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     bad, _, _ = run_reduce(fc, segs, K, dtype, order, rng, opts=opts)
     assert bad == 0
+    # signed zeros, subnormals, infinities and NaNs through the same loads and stack
+    bad, _, _ = run_reduce(fc, segs, K, dtype, order, rng, opts=opts, special=True)
+    assert bad == 0
     assert run_steps(fc, segs, K, dtype, order, rng, steps=2, opts=opts, with_out=True,
                      with_bcast=K <= 64) == 0
 
