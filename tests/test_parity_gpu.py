@@ -625,9 +625,10 @@ def test_sharded_reduction_equals_full_tree(fc, K, S):
 def test_balance_keeps_bits(fc, K, max_blocks, vecs, dtype):
     """fc_plan_balance after every step re-divides the resident tiles among
     the blocks by their XCDs' measured rates: every step before and after
-    stays bit-exact with the oracle (update and raw sum), in one round over
-    8 or 16 blocks (every XCD) and in several rounds (1-3 blocks of 160 tile
-    slots)."""
+    stays bit-exact with the oracle (update, raw sum, and for K <= 16 the
+    broadcast copies), in one round over 8 or 16 blocks (every XCD) and in
+    several rounds (1-3 blocks of 160 tile slots); so does fc_broadcast on
+    the rebalanced ranges."""
     segs = table(16000 + K, dtype, nseg=9)
     segs = segs + [(alloc_len(segs), 150000, 1.0, 1.0)]  # >= 32 tiles per block: launches record
     opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
@@ -640,10 +641,27 @@ def test_balance_keeps_bits(fc, K, max_blocks, vecs, dtype):
         assert info.rounds >= 2
     rates = []
     bad = run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(K), steps=4, opts=opts, with_out=True,
-                    after_step=lambda plan: rates.append(plan.balance()))
+                    with_bcast=K <= 16, after_step=lambda plan: rates.append(plan.balance()))
     assert bad == 0
     ran = [r for r in rates[-1] if r > 0]
     assert 1 <= len(ran) <= min(8, info.grid)
+    # fc_broadcast on rebalanced ranges
+    import torch
+    n = alloc_len(segs)
+    src = host_replicas(np.random.default_rng(K + 1), 1, n, np.float32, special=True)[0]
+    p = fc.Plan(segs, K, dtype, "tree", **opts)
+    reps = to_dev(host_replicas(np.random.default_rng(K + 2), K, n, np.float16 if dtype == "f16" else np.float32))
+    w_d, v_d = torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+    p.step(reps, w_d, v_d, LR, MU, WD, 256)
+    p.balance()
+    kb = K
+    dst = torch.full((K, n), -2.0, device="cuda")
+    p.broadcast(to_dev(src), dst)
+    torch.cuda.synchronize()
+    got = dst[:kb].cpu().numpy()
+    p.close()
+    expect = oracle.broadcast(segs, src, [np.full(n, -2.0, np.float32) for _ in range(kb)])
+    assert sum(same_bits(got[k], expect[k]) for k in range(kb)) == 0
 
 
 def test_balance_full_grid_reduce(fc):
