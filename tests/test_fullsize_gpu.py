@@ -4,7 +4,8 @@ step as bench.py does after its warm-up), on sampled outputs the oracle
 computes one by one.
 
 For each of the five workloads (flat 2^20 x K=4, NiN x K=32, GoogLeNet
-x K=128, VGG-19 x K=16, AlexNet fp16 x K=128) the inputs are drawn on the
+x K=128, VGG-19 x K=16, AlexNet fp16 x K=128), and Table 1's variants
+(GoogLeNet with its auxiliary classifiers, ungrouped AlexNet), the inputs are drawn on the
 device, three fused steps run on the GPU (fc_plan_balance after the first),
 and at every segment's first, second, last and one random element plus 1500
 random elements the oracle recomputes the same three steps from the gathered
@@ -47,7 +48,8 @@ def segment_of(wl, idx):
     return np.searchsorted(offs, idx, side="right") - 1
 
 
-@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "vgg19", "alexnet"])
+@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux",
+                                  "alexnet_ungrouped"])
 def test_fullsize_sampled(fc, name):
     import torch
     wl = tables.get(name)
