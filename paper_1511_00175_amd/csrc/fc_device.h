@@ -428,6 +428,18 @@ __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start,
         off[u] = idx[u] * 4;
     }
     const uint64_t start4 = start * 4;
+    // weights and velocity are loaded before the replica stream, so that
+    // their round trip to memory overlaps the replicas' (measured on MI355X:
+    // a 2^20 x K=4 step in a HIP graph 4.8 vs 5.3 us, fused fp16 K=20 steps
+    // 3-4% faster, fp32 K=9-10 steps equal or up to 1% faster)
+    float w[U][V], v[U][V];
+    if constexpr (MODE == MODE_STEP) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ld32s<V>(gread(a.w) + start4, off[u], w[u]);
+            ld32s<V>(gread(a.v) + start4, off[u], v[u]);
+        }
+    }
     Acc<U, V> s;
     reduce<DT, V, U, C, MAXD, TREE>(a.grads, a.K, start * SG, roff, s);
     if constexpr (MODE == MODE_REDUCE) {
@@ -435,14 +447,6 @@ __device__ __forceinline__ void reduce_body(const ReduceArgs& a, uint64_t start,
         for (int u = 0; u < U; ++u)
             if (act[u]) st32r<V>(gwrite(a.out) + start4, off[u], s.a[u]);
     } else {
-        // weights and velocity are read after the replica stream: loading them
-        // first only holds registers while the sums are being formed
-        float w[U][V], v[U][V];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            ld32s<V>(gread(a.w) + start4, off[u], w[u]);
-            ld32s<V>(gread(a.v) + start4, off[u], v[u]);
-        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (!act[u]) continue;
