@@ -645,12 +645,13 @@ __device__ __forceinline__ void store_slots(const Tile* tiles, float* const* dst
 
 // ------------------------------------------------------------------ resident step
 // One persistent block per CU, for each of the plan's rounds.  Phase 1: wave
-// q of the block reduces tiles lo + q, lo + q + W, ... of its range exactly
-// as reduce_kernel does (same loads, same association) and parks the raw
-// sums in the tile's LDS slot; HBM sees a pure read stream, no writes.
-// Phase 2, after a barrier: the block's threads walk the range again, one
-// wave per tile, and finish each lane-vector from LDS (the SGD update, or
-// the store of the raw sum).  In round r the blocks' ranges are neighbours,
+// q of the block reduces tiles lo + q, lo + q + W, ... of its range in the
+// same association as reduce_kernel (fp32 replicas read as 8-byte pairs,
+// DT = FC_F32_PAIRS) and parks the raw sums in the tile's LDS slot in element
+// order; HBM sees a pure read stream, no writes.  Phase 2, after a barrier:
+// wave q finishes the same tiles from LDS (the SGD update, or the store of
+// the raw sum); with a broadcast, phase 3 stores w' to the K copies one
+// destination at a time (store_slots).  In round r the blocks' ranges are neighbours,
 // so the whole grid streams one region of the parameters at a time.  Blocks
 // share nothing, so the result does not depend on how many of them are
 // resident at once, nor on how the ranges divide the tiles.  Each block
