@@ -108,11 +108,16 @@ int hip_rc(hipError_t e) { return e == hipSuccess ? FC_OK : FC_EHIP; }
 // Replace a device pointer table if its contents differ from the last call.
 // The copy is ordered on `s`; if the previous call ran on another stream,
 // that stream is drained first so that no running kernel still reads the
-// table being replaced.
+// table being replaced.  Not while `s` is being captured into a graph: the
+// graph would record a copy from the plan's host buffer, which later calls
+// overwrite, so a capture may only hold calls that keep the tables.
 template <typename P>
 int update_table(fc_plan* p, std::vector<P>& host, bool& valid, P* dev, const P* want, hipStream_t s) {
     const size_t K = static_cast<size_t>(p->K);
     if (valid && std::equal(host.begin(), host.end(), want)) return FC_OK;
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &capture) != hipSuccess) return FC_EHIP;
+    if (capture != hipStreamCaptureStatusNone) return FC_EINVAL;
     if (p->have_last_stream && p->last_stream != s) {
         if (hipStreamSynchronize(p->last_stream) != hipSuccess) return FC_EHIP;
     }

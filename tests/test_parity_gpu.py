@@ -746,6 +746,89 @@ def test_graph_replays_after_balance(fc):
     pb.close()
 
 
+def test_graph_replays_broadcast(fc):
+    """fc_step with the broadcast and fc_broadcast captured in one HIP graph
+    on a resident plan of several rounds: every replay (eager work and a
+    synchronization between replays, the source changed eagerly each time)
+    gives every destination the oracle's copy of the source and of w'."""
+    import torch
+    segs = table(19000, "f32", nseg=6, max_len=20000)
+    K = 5
+    n = alloc_len(segs)
+    rng = np.random.default_rng(13)
+    reps = to_dev(host_replicas(rng, K, n, np.float32, scale=0.01))
+    w = to_dev(rng.standard_normal(n, dtype=np.float32) * np.float32(0.05))
+    v = torch.zeros(n, device="cuda")
+    src = torch.zeros(n, device="cuda")
+    d1 = torch.full((K, n), -2.0, device="cuda")
+    d2 = torch.full((K, n), -3.0, device="cuda")
+    # one plan per set of destination pointers: a captured call keeps its
+    # plan's pointer tables
+    plan = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=1)
+    pb = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=1)
+    assert plan.info().rounds > 1
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        plan.step(reps, w, v, LR, MU, WD, 256, bcast=d1)
+        pb.broadcast(src, d2)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        plan.step(reps, w, v, LR, MU, WD, 256, bcast=d1)
+        pb.broadcast(src, d2)
+    w_h, v_h = w.cpu().numpy(), v.cpu().numpy()
+    for i in range(3):
+        x = host_replicas(np.random.default_rng(100 + i), 1, n, np.float32, special=True)[0]
+        src.copy_(to_dev(x))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        w_h, v_h, _, _ = oracle.step(segs, list(reps.cpu().numpy()), w_h, v_h, LR, MU, WD, 256)
+        assert same_bits(w.cpu().numpy(), w_h) == 0 and same_bits(v.cpu().numpy(), v_h) == 0
+        want1 = oracle.broadcast(segs, w_h, [np.full(n, -2.0, np.float32) for _ in range(K)])
+        want2 = oracle.broadcast(segs, x, [np.full(n, -3.0, np.float32) for _ in range(K)])
+        got1, got2 = d1.cpu().numpy(), d2.cpu().numpy()
+        assert sum(same_bits(got1[k], want1[k]) for k in range(K)) == 0, i
+        assert sum(same_bits(got2[k], want2[k]) for k in range(K)) == 0, i
+    plan.close()
+    pb.close()
+
+
+def test_capture_refuses_a_table_change(fc):
+    """Inside a graph capture a call whose pointers differ from the plan's
+    previous call returns FC_EINVAL and enqueues nothing; the capture's
+    other calls still replay correctly."""
+    import torch
+    segs = table(20000, "f32", nseg=3, max_len=3000)
+    K = 3
+    n = alloc_len(segs)
+    rng = np.random.default_rng(17)
+    ra = to_dev(host_replicas(rng, K, n, np.float32))
+    rb = ra.clone()
+    out = torch.full((n,), -1.0, device="cuda")
+    plan = fc.Plan(segs, K, "f32", "tree")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        plan.tree_reduce(ra, out)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    codes = []
+    with torch.cuda.graph(g, stream=s):
+        plan.tree_reduce(ra, out)
+        codes.append(fc.fc_tree_reduce(plan.handle, [int(x) for x in fc._rows(rb)], out.data_ptr(),
+                                       s.cuda_stream))
+    assert codes == [fc._fc.FC_EINVAL]
+    out.fill_(-1.0)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    expect = oracle.tree_reduce(segs, list(ra.cpu().numpy()), out=np.full(n, -1.0, np.float32))
+    assert same_bits(out.cpu().numpy(), expect) == 0
+    plan.close()
+
+
 def test_balance_drains_the_plans_stream(fc):
     """Steps on a side stream, fc_plan_balance called with the null stream:
     the call drains the stream the plan last ran on before it replaces the
