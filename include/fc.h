@@ -44,9 +44,9 @@
  *     the plan's previous call, on the same stream, with timing off,
  *     enqueues kernel launches only (no copies, no memsets, no waits), so it
  *     may be captured in a HIP graph; run it once eagerly on the capture
- *     stream first.  A call that would replace a pointer table while its
- *     stream is capturing returns FC_EINVAL and enqueues nothing (use one
- *     plan per set of pointers in a graph).
+ *     stream first.  A call that would replace a pointer table, or that has
+ *     timing on, while its stream is capturing returns FC_EINVAL and
+ *     enqueues nothing (use one plan per set of pointers in a graph).
  *   - Return value: FC_OK (0) or a negative error code (fc_strerror names
  *     it).  Argument errors are detected before anything is enqueued.
  */

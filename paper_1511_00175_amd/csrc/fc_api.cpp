@@ -263,10 +263,15 @@ hipError_t take_event(fc_plan* p, hipEvent_t* e) {
     return hipEventCreate(e);
 }
 
-// Launch `go` on stream s; with timing on, bracket it with two events.
+// Launch `go` on stream s; with timing on, bracket it with two events (not
+// while s is being captured: the plan's records would then name events that
+// only a graph records, so such a call is refused before anything is enqueued).
 template <typename F>
 int launch(fc_plan* p, int kind, hipStream_t s, F&& go) {
     if (!p->timing) return hip_rc(go());
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &capture) != hipSuccess) return FC_EHIP;
+    if (capture != hipStreamCaptureStatusNone) return FC_EINVAL;
     fc_plan::Rec r{nullptr, nullptr, kind};
     if (take_event(p, &r.a) != hipSuccess) return FC_EHIP;
     if (take_event(p, &r.b) != hipSuccess) {

@@ -797,8 +797,9 @@ def test_graph_replays_broadcast(fc):
 
 def test_capture_refuses_a_table_change(fc):
     """Inside a graph capture a call whose pointers differ from the plan's
-    previous call returns FC_EINVAL and enqueues nothing; the capture's
-    other calls still replay correctly."""
+    previous call, or a call with per-kernel timing on, returns FC_EINVAL
+    and enqueues nothing; the capture's other calls still replay
+    correctly."""
     import torch
     segs = table(20000, "f32", nseg=3, max_len=3000)
     K = 3
@@ -815,11 +816,17 @@ def test_capture_refuses_a_table_change(fc):
     s.synchronize()
     g = torch.cuda.CUDAGraph()
     codes = []
+    rows_a = [int(x) for x in fc._rows(ra)]
     with torch.cuda.graph(g, stream=s):
         plan.tree_reduce(ra, out)
         codes.append(fc.fc_tree_reduce(plan.handle, [int(x) for x in fc._rows(rb)], out.data_ptr(),
                                        s.cuda_stream))
-    assert codes == [fc._fc.FC_EINVAL]
+        # per-kernel timing is refused under capture too
+        plan.set_timing(True)
+        codes.append(fc.fc_tree_reduce(plan.handle, rows_a, out.data_ptr(), s.cuda_stream))
+        plan.set_timing(False)
+    assert codes == [fc._fc.FC_EINVAL, fc._fc.FC_EINVAL]
+    assert all(n == 0 for n, _ in plan.read_timing().values())
     out.fill_(-1.0)
     torch.cuda.synchronize()
     g.replay()
