@@ -327,7 +327,8 @@ int fc_plan_read_timing(fc_plan* plan, fc_timing* timing);
  * where the record would cost more than balancing gains, so nothing is
  * recorded -- or that has not launched since it was made or last balanced,
  * is left as it is (FC_OK, rates 0).  Errors: FC_EINVAL (NULL plan,
- * n_rate < 0, or n_rate > 0 with xcd_rate NULL), FC_EHIP, FC_ENOMEM. */
+ * n_rate < 0, n_rate > 0 with xcd_rate NULL, or a stream it would wait on
+ * being captured into a graph), FC_EHIP, FC_ENOMEM. */
 int fc_plan_balance(fc_plan* plan, void* stream, float* xcd_rate, int n_rate);
 
 #ifdef __cplusplus

@@ -105,6 +105,15 @@ int check_aliasing(std::vector<Span>& spans, int out_id, bool f32) {
 
 int hip_rc(hipError_t e) { return e == hipSuccess ? FC_OK : FC_EHIP; }
 
+// FC_OK when `s` is not being captured into a graph; FC_EINVAL when it is
+// (a host wait on it, a table copy or a timed launch would break or corrupt
+// the capture).
+int capture_check(hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &st) != hipSuccess) return FC_EHIP;
+    return st == hipStreamCaptureStatusNone ? FC_OK : FC_EINVAL;
+}
+
 // Replace a device pointer table if its contents differ from the last call.
 // The copy is ordered on `s`; if the previous call ran on another stream,
 // that stream is drained first so that no running kernel still reads the
@@ -115,10 +124,11 @@ template <typename P>
 int update_table(fc_plan* p, std::vector<P>& host, bool& valid, P* dev, const P* want, hipStream_t s) {
     const size_t K = static_cast<size_t>(p->K);
     if (valid && std::equal(host.begin(), host.end(), want)) return FC_OK;
-    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s, &capture) != hipSuccess) return FC_EHIP;
-    if (capture != hipStreamCaptureStatusNone) return FC_EINVAL;
+    int rc = capture_check(s);
+    if (rc) return rc;
     if (p->have_last_stream && p->last_stream != s) {
+        rc = capture_check(p->last_stream);
+        if (rc) return rc;
         if (hipStreamSynchronize(p->last_stream) != hipSuccess) return FC_EHIP;
     }
     host.assign(want, want + K);
@@ -269,9 +279,8 @@ hipError_t take_event(fc_plan* p, hipEvent_t* e) {
 template <typename F>
 int launch(fc_plan* p, int kind, hipStream_t s, F&& go) {
     if (!p->timing) return hip_rc(go());
-    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s, &capture) != hipSuccess) return FC_EHIP;
-    if (capture != hipStreamCaptureStatusNone) return FC_EINVAL;
+    const int crc = capture_check(s);
+    if (crc) return crc;
     fc_plan::Rec r{nullptr, nullptr, kind};
     if (take_event(p, &r.a) != hipSuccess) return FC_EHIP;
     if (take_event(p, &r.b) != hipSuccess) {
@@ -566,6 +575,11 @@ static int fc_plan_balance_body(fc_plan* p, void* stream, float* xcd_rate, int n
     if (p->schedule != FC_SCHED_RESIDENT || !p->res_record) return FC_OK;
     // no launch of this plan may still read the range table or write the
     // record: drain the given stream and the stream of the plan's last call
+    // (neither may be capturing: a host wait would break the capture)
+    const hipStream_t given = static_cast<hipStream_t>(stream);
+    int crc = capture_check(given);
+    if (!crc && p->have_last_stream && p->last_stream != given) crc = capture_check(p->last_stream);
+    if (crc) return crc;
     if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess ||
         (p->have_last_stream && p->last_stream != static_cast<hipStream_t>(stream) &&
          hipStreamSynchronize(p->last_stream) != hipSuccess))

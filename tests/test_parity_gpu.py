@@ -836,6 +836,41 @@ def test_capture_refuses_a_table_change(fc):
     plan.close()
 
 
+def test_balance_refused_under_capture(fc):
+    """fc_plan_balance would wait on the stream: while that stream is being
+    captured it returns FC_EINVAL without waiting, the capture stays valid
+    and its step replays bit-exact with an eager twin plan."""
+    import torch
+    segs = table(18000, "f32", nseg=9)  # 110 tiles, 55 per block of 2: launches record
+    K = 24
+    n = alloc_len(segs)
+    rng = np.random.default_rng(19)
+    reps = to_dev(host_replicas(rng, K, n, np.float32, scale=0.01))
+    w0 = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+    wa, va = to_dev(w0), torch.zeros(n, device="cuda")
+    wb, vb = to_dev(w0), torch.zeros(n, device="cuda")
+    pa = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=2)
+    pb = fc.Plan(segs, K, "f32", "tree", schedule=3, max_blocks=2)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+    s.synchronize()
+    pb.step(reps, wb, vb, LR, MU, WD, 256)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        pa.step(reps, wa, va, LR, MU, WD, 256)
+        rc, _ = fc.fc_plan_balance(pa.handle, s.cuda_stream)
+    assert rc == fc._fc.FC_EINVAL
+    g.replay()
+    pb.step(reps, wb, vb, LR, MU, WD, 256)
+    torch.cuda.synchronize()
+    assert same_bits(wa.cpu().numpy(), wb.cpu().numpy()) == 0
+    assert same_bits(va.cpu().numpy(), vb.cpu().numpy()) == 0
+    pa.close()
+    pb.close()
+
+
 def test_balance_drains_the_plans_stream(fc):
     """Steps on a side stream, fc_plan_balance called with the null stream:
     the call drains the stream the plan last ran on before it replaces the
