@@ -193,7 +193,7 @@ def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
         m = m2
     bytes_ = n * (wl.K * wl.s_g + 16)
     model, ncpu = host_info()
-    # the machine's CPU share: OMP_NUM_THREADS when set, else every core
+    # the host's CPU share: OMP_NUM_THREADS when set, else every core
     nthreads = max(1, min(ncpu or 1, int(os.environ.get("OMP_NUM_THREADS", ncpu or 1))))
     dt_mt = run_threads(m, nthreads)
     return {"value": round(bytes_ / dt_mt / 1e9, 4), "unit": "GB/s", "cores": nthreads, "kind": "oracle",
@@ -381,7 +381,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU only (the K workers are replicas on one device); "
+        print("bench.py: this benchmark measures one GPU only (the K workers are replicas on one device); "
               "--gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
