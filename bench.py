@@ -511,7 +511,7 @@ def main():
                  args.no_balance or args.wv_sets)
     traffic = read_traffic(wl.name, dom) if plain else None
     sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
-    rk = "ksplit_kernel" if info.k_waves > 1 else "resident_kernel" if info.schedule == 3 else "reduce_kernel"
+    rk = "resident_kernel" if info.schedule == 3 else "reduce_kernel"
 
     res = {
         "metric": METRIC,
@@ -535,7 +535,7 @@ def main():
             "write_sum": args.out, "broadcast": args.bcast,
             "algorithmic_bytes_per_step": bytes_step,
             "launch": {"grid": info.grid, "tiles": info.ntiles, "block_threads": info.block_threads,
-                       "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk, "k_waves": info.k_waves,
+                       "vecs_per_thread": info.vecs_per_thread, "kchunk": info.kchunk,
                        "schedule": sched, "rounds": info.rounds, "lds_bytes": info.lds_bytes},
             "input_sets": args.rotate,
             "w_v_sets": n_wv,

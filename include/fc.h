@@ -35,16 +35,22 @@
  *     belong to no segment are never written.
  *   - Every pointer must be 16-byte aligned (FC_EALIGN otherwise).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
- *     stream) and never synchronize the host, except when a replica or
- *     destination pointer table differs from the plan's previous call and
- *     that call was on another stream (the library then waits for that
- *     stream before replacing the table).  Calls on one plan must not run
- *     concurrently from several host threads.
+ *     stream) and do not wait on the host (fc_plan_balance and
+ *     fc_plan_read_timing do).  A call whose replica or destination pointers
+ *     differ from the plan's previous call copies the new pointer table from
+ *     host memory (the HIP runtime may finish that copy before returning).
+ *     Calls on one plan must not run concurrently from several host threads.
+ *   - Calls on one plan take effect in the order they are made, whatever
+ *     their streams: a call on another stream than the plan's previous call
+ *     first makes its stream wait, on the device, for the work enqueued so
+ *     far on that previous stream (which must still exist), so the plan's
+ *     tables and scratch never serve two calls at once.
  *   - Graph capture: a call whose replica and destination pointers equal
- *     the plan's previous call, on the same stream, with timing off,
- *     enqueues kernel launches only (no copies, no memsets, no waits), so it
- *     may be captured in a HIP graph; run it once eagerly on the capture
- *     stream first.  A call that would replace a pointer table, or that has
+ *     the plan's previous call, with timing off, enqueues kernel launches
+ *     only (no copies, no memsets, no waits), so it may be captured in a HIP
+ *     graph; run it once eagerly first.  Whoever launches the graph orders
+ *     its calls: a captured call neither waits for the plan's previous call
+ *     nor becomes it.  A call that would replace a pointer table, or that has
  *     timing on, while its stream is capturing returns FC_EINVAL and
  *     enqueues nothing (use one plan per set of pointers in a graph).
  *   - Return value: FC_OK (0) or a negative error code (fc_strerror names
@@ -105,7 +111,7 @@ typedef struct fc_plan fc_plan;
  *   per round.  It also
  *   makes fc_tree_reduce store the sums only after each read phase.  Tiles of
  *   64 lanes x 1 vector with batches of 16 replicas (default), or x 2 vectors
- *   with batches of 4 (vecs_per_thread 2, K < 512); no K split.
+ *   with batches of 4 (vecs_per_thread 2, K < 512).
  * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
  *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
  *   round holds the plan or a parameter's replicas take at least 48 bytes
@@ -123,11 +129,9 @@ typedef enum {
  * schedule, the replica type, K and the plan's size (measured on MI355X):
  * RESIDENT -> 64-lane tiles of (2 vectors, batches of 4 replicas) for fp32
  * replicas with K <= 16, else (1 vector, batches of 16); vecs_per_thread and
- * kchunk may name either; otherwise fp32 in tree
- * order with 16 <= K <= 48 and at least 2^25 parameters -> K split over 8
- * waves (see k_waves); fp16 -> (4 vectors, 4 replicas, 256 threads); fp32 with
- * 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads
- * always carry the streaming (nt) hint. */
+ * kchunk may name either; otherwise fp16 -> (4 vectors, 4 replicas, 256
+ * threads); fp32 with 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16,
+ * 64).  Replica loads always carry the streaming (nt) hint. */
 typedef struct {
     int block_threads;   /* 64, 128 or 256 threads per block */
     int vecs_per_thread; /* 4-element lane-vectors per thread (1, 2 or 4) ... */
@@ -135,19 +139,9 @@ typedef struct {
                             (1, 8) (1, 16) (2, 8) (2, 16) (4, 2) (4, 4) (4, 8) */
     int max_blocks;      /* cap on the grid; blocks then loop over tiles (default: no cap) */
     int schedule;        /* fc_schedule of fc_step (default FC_SCHED_AUTO) */
-    int k_waves;         /* tree order only: 4, 8 or 16 waves of a block split the K
-                            replicas between them (block_threads 64 * k_waves;
-                            wave q reduces an aligned run of replicas, a complete
-                            subtree of the tree, and the block combines the runs
-                            in tree order through LDS).
-                            Compiled (k_waves, vecs_per_thread, kchunk): (4, 4, 2)
-                            (8, 4, 2) (16, 4, 2) (8, 2, 4) (16, 2, 4) (16, 2, 2); a
-                            wave's run may span at most 8 batches of kchunk
-                            (K <= 8 * kchunk * k_waves), else FC_EINVAL.  With a
-                            split, vecs_per_thread and kchunk default to 4 and 2.
-                            1: no split.
-                            0: the default, or no split when another shape field
-                            is given. */
+    int k_waves;         /* 0 or 1: one wave reduces all K replicas of each of its
+                            lane-vectors (other values are FC_EINVAL); 1 counts
+                            as a launch-shape field for AUTO */
 } fc_launch_opts;
 
 /* Create a plan for K workers over a segment table (Sec. 6: one gradient
@@ -280,7 +274,7 @@ typedef struct {
     int kchunk;
     int schedule;        /* resolved fc_schedule of fc_step: FUSED, TWO_PASS or RESIDENT */
     uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
-    int k_waves;         /* waves splitting the K replicas (1: no split) */
+    int k_waves;         /* always 1: one wave reduces all K replicas of a lane-vector */
     int lds_bytes;       /* RESIDENT: LDS per block (0 for the other schedules) */
     int rounds;          /* RESIDENT: rounds of the persistent grid (0 otherwise) */
 } fc_plan_info;

@@ -9,10 +9,11 @@ The work is done by HIP kernels behind the C ABI of include/fc.h; this package
 only marshals torch tensors (device memory and the current stream) into it.
 """
 from . import _fc
-from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO, FC_SCHED_FUSED,  # noqa: F401
-                  FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query,
-                  fc_lr_at, fc_plan_balance, fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks,
-                  fc_sgd_step, fc_step, fc_strerror, fc_train, fc_tree_reduce, lr_policy)
+from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO,  # noqa: F401
+                  FC_SCHED_FUSED, FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create,
+                  fc_plan_destroy, fc_plan_query, fc_lr_at, fc_plan_balance, fc_plan_read_timing, fc_plan_set_timing,
+                  fc_read_probe, fc_read_probe_blocks, fc_sgd_step, fc_step, fc_strerror, fc_train,
+                  fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
            "fc_plan_read_timing", "fc_plan_balance", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
@@ -63,6 +64,26 @@ def _rows(x):
     return [base + k * step for k in range(x.shape[0])]
 
 
+_TORCH_DTYPES = {"f32": "float32", "f16": "float16"}
+
+
+def _check_vector(t, name, dtype, device, n):
+    """`t` must be a contiguous torch tensor of `dtype` on `device` holding at
+    least n elements (the C ABI sees only the pointer, so a short or
+    mistyped buffer would be read or written out of bounds on the GPU)."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if t.dtype != getattr(torch, dtype):
+        raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the plan on {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < n:
+        raise ValueError(f"{name} holds {t.numel()} elements, the plan covers {n}")
+
+
 class Plan:
     """One segment table and worker count (fc_plan).
 
@@ -75,6 +96,7 @@ class Plan:
     """
 
     def __init__(self, segments, K, dtype="f32", order="tree", **opts):
+        import torch
         rc, h = fc_plan_create(segments, K, _DTYPES[dtype], _ORDERS[order], opts or None)
         if rc:
             raise FcError("fc_plan_create", rc)
@@ -82,6 +104,44 @@ class Plan:
         self.K = K
         self.dtype = dtype
         self.order = order
+        # what every buffer passed to the plan must cover, and where
+        self.extent = fc_plan_query(h).extent
+        self.device = torch.device("cuda", torch.cuda.current_device())
+
+    def _vec(self, t, name, optional=False):
+        """Pointer of an fp32 buffer (w, v, out, g, src) after checking it."""
+        if t is None and optional:
+            return None
+        _check_vector(t, name, "float32", self.device, self.extent)
+        return t.data_ptr()
+
+    def _reps(self, x, name, dtype):
+        """Pointers of K buffers (replicas of the plan's type, or fp32
+        broadcast destinations): a list of K tensors or a 2-D tensor of K
+        rows, each checked like _vec."""
+        import torch
+        if isinstance(x, (list, tuple)):
+            if len(x) != self.K:
+                raise ValueError(f"{name}: {len(x)} buffers for a plan of K={self.K}")
+            for k, t in enumerate(x):
+                _check_vector(t, f"{name}[{k}]", dtype, self.device, self.extent)
+            return [t.data_ptr() for t in x]
+        if not isinstance(x, torch.Tensor) or x.dim() != 2:
+            raise ValueError(f"{name} must be a list of K tensors or a 2-D tensor of K rows")
+        if x.shape[0] != self.K:
+            raise ValueError(f"{name} has {x.shape[0]} rows for a plan of K={self.K}")
+        if x.stride(1) != 1 or (self.K > 1 and x.stride(0) < x.shape[1]):
+            raise ValueError(f"{name} must be row-major with rows that do not overlap")
+        if x.shape[1] < self.extent:
+            raise ValueError(f"{name} rows hold {x.shape[1]} elements, the plan covers {self.extent}")
+        if x.dtype != getattr(torch, dtype):
+            raise ValueError(f"{name} must be {dtype}, not {x.dtype}")
+        if x.device != self.device:
+            raise ValueError(f"{name} is on {x.device}, the plan on {self.device}")
+        return _rows(x)
+
+    def _grads(self, x):
+        return self._reps(x, "grads", _TORCH_DTYPES[self.dtype])
 
     def close(self):
         if self.handle:
@@ -116,30 +176,36 @@ class Plan:
         return rates
 
     def tree_reduce(self, grads, out, stream=None):
-        rc = fc_tree_reduce(self.handle, _rows(grads), _ptr(out), _stream(stream))
+        rc = fc_tree_reduce(self.handle, self._grads(grads), self._vec(out, "out"), _stream(stream))
         if rc:
             raise FcError("fc_tree_reduce", rc)
 
     def sgd_step(self, w, v, g, lr, mu, wd, batch, stream=None):
-        rc = fc_sgd_step(self.handle, _ptr(w), _ptr(v), _ptr(g), lr, mu, wd, batch, _stream(stream))
+        rc = fc_sgd_step(self.handle, self._vec(w, "w"), self._vec(v, "v"), self._vec(g, "g"), lr, mu, wd, batch,
+                         _stream(stream))
         if rc:
             raise FcError("fc_sgd_step", rc)
 
     def broadcast(self, src, dst, stream=None):
-        rc = fc_broadcast(self.handle, _ptr(src), _rows(dst), _stream(stream))
+        rc = fc_broadcast(self.handle, self._vec(src, "src"), self._reps(dst, "dst", "float32"), _stream(stream))
         if rc:
             raise FcError("fc_broadcast", rc)
 
     def train(self, grads, w, v, policy, first_iter, n_iters, mu, wd, batch, stream=None):
         """n_iters fused steps with the policy's rate (policy: lr_policy
         keyword arguments); the same replicas feed every step."""
-        rc = fc_train(self.handle, _rows(grads), _ptr(w), _ptr(v), lr_policy(**policy), first_iter, n_iters,
-                      mu, wd, batch, _stream(stream))
+        rc = fc_train(self.handle, self._grads(grads), self._vec(w, "w"), self._vec(v, "v"), lr_policy(**policy),
+                      first_iter, n_iters, mu, wd, batch, _stream(stream))
         if rc:
             raise FcError("fc_train", rc)
 
+    def _step_args(self, grads, w, v, out, bcast):
+        return (self._grads(grads), self._vec(w, "w"), self._vec(v, "v"), self._vec(out, "out", optional=True),
+                None if bcast is None else self._reps(bcast, "bcast", "float32"))
+
     def step(self, grads, w, v, lr, mu, wd, batch, out=None, bcast=None, stream=None):
-        rc = fc_step(self.handle, _rows(grads), _ptr(w), _ptr(v), lr, mu, wd, batch, _ptr(out),
-                     None if bcast is None else _rows(bcast), _stream(stream))
+        g, wp, vp, op, bp = self._step_args(grads, w, v, out, bcast)
+        rc = fc_step(self.handle, g, wp, vp, lr, mu, wd, batch, op, bp, _stream(stream))
         if rc:
             raise FcError("fc_step", rc)
+

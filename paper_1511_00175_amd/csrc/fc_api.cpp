@@ -62,8 +62,9 @@ struct fc_plan {
     std::vector<float*> h_dst;
     bool grads_valid = false;
     bool dst_valid = false;
-    hipStream_t last_stream = nullptr;
+    hipStream_t last_stream = nullptr;  // stream of the plan's previous (uncaptured) call
     bool have_last_stream = false;
+    hipEvent_t order_event = nullptr;    // orders a call on another stream after the previous one
 };
 
 namespace {
@@ -74,9 +75,18 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 struct Span {
     uintptr_t lo, hi;  // [lo, hi)
-    bool written;
     int id;            // distinct buffer id; replicas share role 0 and differ by id
+    bool written;
     bool replica;
+};
+
+// The buffers one call names (at most K replicas, K destinations and four
+// more), held on the caller's stack so that validation allocates nothing.
+struct Spans {
+    static constexpr int CAP = 2 * K_MAX + 4;
+    Span v[CAP];
+    int n = 0;
+    void push(const Span& x) { v[n++] = x; }
 };
 
 // Written buffers may not overlap any other buffer, except that `out` may be
@@ -84,11 +94,11 @@ struct Span {
 // that writes it).  Read-only buffers may overlap each other.  The spans are
 // sorted by start and each is compared only with the spans that start
 // before it ends, so a valid call costs O(n log n) for n = K + a few spans.
-int check_aliasing(std::vector<Span>& spans, int out_id, bool f32) {
-    spans.erase(std::remove_if(spans.begin(), spans.end(), [](const Span& x) { return x.hi == x.lo; }),
-                spans.end());
-    std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.lo < y.lo; });
-    const size_t n = spans.size();
+int check_aliasing(Spans& sp, int out_id, bool f32) {
+    Span* spans = sp.v;
+    const size_t n =
+        static_cast<size_t>(std::remove_if(spans, spans + sp.n, [](const Span& x) { return x.hi == x.lo; }) - spans);
+    std::sort(spans, spans + n, [](const Span& x, const Span& y) { return x.lo < y.lo; });
     for (size_t i = 0; i < n; ++i) {
         const Span& a = spans[i];
         for (size_t j = i + 1; j < n && spans[j].lo < a.hi; ++j) {
@@ -114,23 +124,49 @@ int capture_check(hipStream_t s) {
     return st == hipStreamCaptureStatusNone ? FC_OK : FC_EINVAL;
 }
 
+// Calls on one plan take effect in the order they are made, whatever their
+// streams.  A call on another stream than the plan's previous call first
+// makes its stream wait, on the device, for everything enqueued so far on
+// the previous call's stream (one event recorded there), so the plan's
+// shared device state -- pointer tables, the two-pass raw-sum scratch, the
+// resident launch record -- never serves two calls at once and the host
+// never waits.  A call enqueued while its stream is being captured into a
+// graph runs when the graph is launched, which its launcher orders: it
+// neither waits nor becomes the previous call.  Sets `note` when the call
+// becomes the plan's previous call (note_stream once it has enqueued).
+int order_after_last(fc_plan* p, hipStream_t s, bool& note) {
+    note = false;
+    if (p->have_last_stream && p->last_stream == s) return FC_OK;
+    int rc = capture_check(s);
+    if (rc == FC_EINVAL) return FC_OK;  // being captured
+    if (rc) return rc;
+    note = true;
+    if (!p->have_last_stream) return FC_OK;
+    // the previous stream's pending work cannot be named by an event recorded
+    // outside a capture it has since joined
+    rc = capture_check(p->last_stream);
+    if (rc) return rc;
+    if (!p->order_event && hipEventCreateWithFlags(&p->order_event, hipEventDisableTiming) != hipSuccess)
+        return FC_EHIP;
+    if (hipEventRecord(p->order_event, p->last_stream) != hipSuccess ||
+        hipStreamWaitEvent(s, p->order_event, 0) != hipSuccess)
+        return FC_EHIP;
+    return FC_OK;
+}
+
 // Replace a device pointer table if its contents differ from the last call.
-// The copy is ordered on `s`; if the previous call ran on another stream,
-// that stream is drained first so that no running kernel still reads the
-// table being replaced.  Not while `s` is being captured into a graph: the
-// graph would record a copy from the plan's host buffer, which later calls
-// overwrite, so a capture may only hold calls that keep the tables.
+// The copy is ordered on `s` after every earlier call of the plan
+// (order_after_last ran first).  Not while `s` is being captured into a
+// graph: the graph would record a copy from the plan's host buffer, which
+// later calls overwrite, so a capture may only hold calls that keep the
+// tables.  `host` has K entries from plan creation on, so assigning K new
+// ones allocates nothing.
 template <typename P>
 int update_table(fc_plan* p, std::vector<P>& host, bool& valid, P* dev, const P* want, hipStream_t s) {
     const size_t K = static_cast<size_t>(p->K);
     if (valid && std::equal(host.begin(), host.end(), want)) return FC_OK;
-    int rc = capture_check(s);
+    const int rc = capture_check(s);
     if (rc) return rc;
-    if (p->have_last_stream && p->last_stream != s) {
-        rc = capture_check(p->last_stream);
-        if (rc) return rc;
-        if (hipStreamSynchronize(p->last_stream) != hipSuccess) return FC_EHIP;
-    }
     host.assign(want, want + K);
     valid = false;
     if (hipMemcpyAsync(dev, host.data(), K * sizeof(P), hipMemcpyHostToDevice, s) != hipSuccess)
@@ -178,62 +214,36 @@ void note_stream(fc_plan* p, hipStream_t s) {
     p->have_last_stream = true;
 }
 
-int validate_opts(const fc_launch_opts* o, fc_dtype gdt, fc_order order, int K, uint64_t n_elems,
-                  fc::Shape& sh, bool& shape_given) {
+int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh, bool& shape_given) {
     fc::default_shape(gdt, K, sh);
-    int w = fc::default_kwaves(gdt, order, K, n_elems);
-    int u = 4, c = 2;  // lane vectors and batch of a K split
     shape_given = false;
     if (o) {
-        if (o->k_waves < 0 || o->max_blocks < 0) return FC_EINVAL;
+        // k_waves: one wave reduces all K replicas of its lane-vectors (0 or 1)
+        if (o->k_waves < 0 || o->k_waves > 1 || o->max_blocks < 0) return FC_EINVAL;
         if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_RESIDENT) return FC_EINVAL;
-        // an explicit shape without k_waves asks for the unsplit kernel
         shape_given = o->block_threads || o->vecs_per_thread || o->kchunk || o->k_waves;
         if (o->schedule == FC_SCHED_RESIDENT) {
             // the resident kernel's tiles: 64 lanes of (1 vector, batches of 16)
-            // or (2 vectors, batches of 4); no K split.  The plan sets the shape.
+            // or (2 vectors, batches of 4).  The plan sets the shape.
             const int ru = o->vecs_per_thread ? o->vecs_per_thread : 1;
             const int rc = o->kchunk ? o->kchunk : (ru == 2 ? 4 : 16);
-            if (o->k_waves > 1 || (o->block_threads && o->block_threads != 64) || !fc::resident_pair(ru, rc) ||
+            if ((o->block_threads && o->block_threads != 64) || !fc::resident_pair(ru, rc) ||
                 !fc::resident_fits_k(ru, rc, K))
                 return FC_EINVAL;
-            sh.kwaves = 1;
             return FC_OK;
         }
-        if (o->k_waves) w = o->k_waves;
-        else if (shape_given) w = 1;
-        if (w > 1) {
-            if (o->vecs_per_thread) u = o->vecs_per_thread;
-            if (o->kchunk) c = o->kchunk;
-            if (o->block_threads && o->block_threads != 64 * w) return FC_EINVAL;
-        } else {
-            if (o->block_threads) {
-                if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
-                sh.block = o->block_threads;
-            }
-            if (o->vecs_per_thread || o->kchunk) {
-                // an explicit pair replaces the default pair; one field alone keeps the other default
-                const int pu = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
-                const int pc = o->kchunk ? o->kchunk : sh.kchunk;
-                if (!fc::compiled_pair(pu, pc)) return FC_EINVAL;
-                sh.vecs = pu;
-                sh.kchunk = pc;
-            }
+        if (o->block_threads) {
+            if (o->block_threads != 64 && o->block_threads != 128 && o->block_threads != 256) return FC_EINVAL;
+            sh.block = o->block_threads;
         }
-    }
-    if (w > 1) {
-        if (order != FC_ORDER_TREE || !fc::compiled_ksplit(w, u, c)) return FC_EINVAL;
-        sh.kwaves = w;
-        sh.vecs = u;
-        sh.kchunk = c;
-        sh.block = 64 * w;
-        sh.span = fc::ksplit_span(K, w, c);
-        if (sh.span / c > fc::KSPLIT_MAX_BATCHES) return FC_EINVAL;
-        sh.lanes = 64;
-    } else {
-        sh.kwaves = 1;
-        sh.span = K;
-        sh.lanes = sh.block;
+        if (o->vecs_per_thread || o->kchunk) {
+            // an explicit pair replaces the default pair; one field alone keeps the other default
+            const int pu = o->vecs_per_thread ? o->vecs_per_thread : sh.vecs;
+            const int pc = o->kchunk ? o->kchunk : sh.kchunk;
+            if (!fc::compiled_pair(pu, pc)) return FC_EINVAL;
+            sh.vecs = pu;
+            sh.kchunk = pc;
+        }
     }
     return FC_OK;
 }
@@ -254,6 +264,7 @@ void free_plan(fc_plan* p) {
         (void)hipEventDestroy(r.b);
     }
     for (auto e : p->event_pool) (void)hipEventDestroy(e);
+    if (p->order_event) (void)hipEventDestroy(p->order_event);
     if (p->d_sum) (void)hipFree(p->d_sum);
     if (p->d_ranges) (void)hipFree(p->d_ranges);
     if (p->d_clock) (void)hipFree(p->d_clock);
@@ -364,7 +375,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     if (end > (UINT64_MAX / 8)) return FC_EINVAL;
     fc::Shape sh{};
     bool shape_given = false;
-    int rc = validate_opts(opts, gdt, order, K, n_elems, sh, shape_given);
+    int rc = validate_opts(opts, gdt, K, sh, shape_given);
     if (rc) return rc;
     const int sched_req = opts ? opts->schedule : FC_SCHED_AUTO;
 
@@ -414,9 +425,6 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         sh.block = 64;
         sh.vecs = res_u;
         sh.kchunk = res_c;
-        sh.kwaves = 1;
-        sh.span = K;
-        sh.lanes = 64;
     }
 
     fc_plan* p = new (std::nothrow) fc_plan();
@@ -430,23 +438,21 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     p->extent = end;
     sh.dtype = gdt;
     sh.tree = order == FC_ORDER_TREE;
-    const int need = bit_length(K / sh.kchunk);
-    if (sh.kwaves == 1 && need > fc::MAXD_MAX) {
+    sh.maxd = bit_length(K / sh.kchunk);
+    if (sh.maxd > fc::MAXD_MAX) {
         delete p;
         return FC_EINVAL;
     }
-    // with a K split: the depth a wave's run of span / kchunk batches needs
-    sh.maxd = sh.kwaves == 1 ? need : bit_length(sh.span / sh.kchunk);
     p->shape = sh;
 
-    // Tile map: each segment is cut into tiles of at most lanes*vecs vectors;
+    // Tile map: each segment is cut into tiles of at most block*vecs vectors;
     // a length that is not a multiple of the vector width leaves a tail tile.
     std::vector<Tile> tiles;
     std::vector<float> mults;
     try {
         p->segs.assign(segs, segs + nseg);
         mults.resize(2 * static_cast<size_t>(std::max(nseg, 1)));
-        const uint64_t tile_vecs = static_cast<uint64_t>(sh.lanes) * sh.vecs;
+        const uint64_t tile_vecs = static_cast<uint64_t>(sh.block) * sh.vecs;
         for (int j = 0; j < nseg; ++j) {
             const fc_segment& s = segs[j];
             mults[2 * j] = s.lr_mult;
@@ -558,7 +564,7 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->kchunk = p->shape.kchunk;
     info->schedule = p->schedule;
     info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
-    info->k_waves = p->shape.kwaves;
+    info->k_waves = 1;
     info->lds_bytes = p->schedule == FC_SCHED_RESIDENT ? p->res_lds : 0;
     info->rounds = p->schedule == FC_SCHED_RESIDENT ? p->res_rounds : 0;
     if (p->schedule == FC_SCHED_RESIDENT) {
@@ -663,26 +669,26 @@ namespace {
 // Byte extent of a buffer of `elem` bytes per element covering the plan.
 Span span_of(const fc_plan* p, const void* ptr, int elem, bool written, int id, bool replica) {
     const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
-    return Span{lo, lo + static_cast<uintptr_t>(p->extent) * elem, written, id, replica};
+    return Span{lo, lo + static_cast<uintptr_t>(p->extent) * elem, id, written, replica};
 }
 
 enum { ID_W = 1, ID_V, ID_OUT, ID_G, ID_SRC, ID_REPLICA0 = 16 };
 
-int check_replicas(const fc_plan* p, const void* const* grads, std::vector<Span>& spans) {
+int check_replicas(const fc_plan* p, const void* const* grads, Spans& spans) {
     if (!grads) return FC_EINVAL;
     for (int k = 0; k < p->K; ++k) {
         if (!grads[k]) return FC_EINVAL;
         if (!aligned16(grads[k])) return FC_EALIGN;
-        spans.push_back(span_of(p, grads[k], p->sg, false, ID_REPLICA0 + k, true));
+        spans.push(span_of(p, grads[k], p->sg, false, ID_REPLICA0 + k, true));
     }
     return FC_OK;
 }
 
-int check_dsts(const fc_plan* p, float* const* dst, std::vector<Span>& spans) {
+int check_dsts(const fc_plan* p, float* const* dst, Spans& spans) {
     for (int k = 0; k < p->K; ++k) {
         if (!dst[k]) return FC_EINVAL;
         if (!aligned16(dst[k])) return FC_EALIGN;
-        spans.push_back(span_of(p, dst[k], 4, true, ID_REPLICA0 + p->K + k, false));
+        spans.push(span_of(p, dst[k], 4, true, ID_REPLICA0 + p->K + k, false));
     }
     return FC_OK;
 }
@@ -692,29 +698,32 @@ int check_dsts(const fc_plan* p, float* const* dst, std::vector<Span>& spans) {
 static int fc_tree_reduce_body(fc_plan* p, const void* const* grads, float* out, void* stream) {
     if (!p || !out) return FC_EINVAL;
     if (!aligned16(out)) return FC_EALIGN;
-    std::vector<Span> spans;
+    Spans spans;
     int rc = check_replicas(p, grads, spans);
     if (rc) return rc;
-    spans.push_back(span_of(p, out, 4, true, ID_OUT, false));
+    spans.push(span_of(p, out, 4, true, ID_OUT, false));
     rc = check_aliasing(spans, ID_OUT, p->gdt == FC_F32);
     if (rc) return rc;
     if (p->ntiles == 0) return FC_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    bool note = false;
+    rc = order_after_last(p, s, note);
     if (rc) return rc;
-    fc::ReduceArgs a{};
-    a.tiles = p->d_tiles;
-    a.ntiles = p->ntiles;
-    a.mults = p->d_mults;
-    a.grads = p->d_grads;
-    a.K = p->K;
-    a.span = p->shape.span;
-    a.out = out;
-    rc = launch(p, FC_KERNEL_REDUCE, s, [&] {
-        return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_REDUCE, a, s)
-                                                : launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s);
-    });
-    note_stream(p, s);
+    rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    if (rc == FC_OK) {
+        fc::ReduceArgs a{};
+        a.tiles = p->d_tiles;
+        a.ntiles = p->ntiles;
+        a.mults = p->d_mults;
+        a.grads = p->d_grads;
+        a.K = p->K;
+        a.out = out;
+        rc = launch(p, FC_KERNEL_REDUCE, s, [&] {
+            return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_REDUCE, a, s)
+                                                    : launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, a, s);
+        });
+    }
+    if (note) note_stream(p, s);
     return rc;
 }
 
@@ -722,12 +731,17 @@ static int fc_sgd_step_body(fc_plan* p, float* w, float* v, const float* g, floa
                 void* stream) {
     if (!p || !w || !v || !g || batch < 1) return FC_EINVAL;
     if (!aligned16(w) || !aligned16(v) || !aligned16(g)) return FC_EALIGN;
-    std::vector<Span> spans = {span_of(p, w, 4, true, ID_W, false), span_of(p, v, 4, true, ID_V, false),
-                               span_of(p, g, 4, false, ID_G, false)};
+    Spans spans;
+    spans.push(span_of(p, w, 4, true, ID_W, false));
+    spans.push(span_of(p, v, 4, true, ID_V, false));
+    spans.push(span_of(p, g, 4, false, ID_G, false));
     int rc = check_aliasing(spans, -1, false);
     if (rc) return rc;
     if (p->ntiles == 0) return FC_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    bool note = false;
+    rc = order_after_last(p, s, note);
+    if (rc) return rc;
     fc::SgdArgs a{};
     a.tiles = p->d_tiles;
     a.ntiles = p->ntiles;
@@ -740,119 +754,146 @@ static int fc_sgd_step_body(fc_plan* p, float* w, float* v, const float* g, floa
     a.wd = wd;
     a.c = 1.0f / static_cast<float>(batch);
     rc = launch(p, FC_KERNEL_SGD, s, [&] { return fc::launch_sgd(p->shape, p->grid, a, s); });
-    note_stream(p, s);
+    if (note) note_stream(p, s);
     return rc;
 }
 
 static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, void* stream) {
     if (!p || !src || !dst) return FC_EINVAL;
     if (!aligned16(src)) return FC_EALIGN;
-    std::vector<Span> spans = {span_of(p, src, 4, false, ID_SRC, false)};
+    Spans spans;
+    spans.push(span_of(p, src, 4, false, ID_SRC, false));
     int rc = check_dsts(p, dst, spans);
     if (rc) return rc;
     rc = check_aliasing(spans, -1, false);
     if (rc) return rc;
     if (p->ntiles == 0) return FC_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, dst, s);
+    bool note = false;
+    rc = order_after_last(p, s, note);
     if (rc) return rc;
-    fc::BcastArgs a{};
-    a.tiles = p->d_tiles;
-    a.ntiles = p->ntiles;
-    a.src = src;
-    a.dst = p->d_dst;
-    a.K = p->K;
-    rc = launch(p, FC_KERNEL_BCAST, s, [&] {
-        if (p->schedule != FC_SCHED_RESIDENT) return fc::launch_bcast(p->shape, p->grid, a, s);
-        // resident plans: the step's ranges, one launch per round
-        for (int round = 0; round < p->res_rounds; ++round) {
-            a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
-            const hipError_t e =
-                fc::launch_resident_bcast(p->shape, p->res_grid, static_cast<size_t>(p->res_lds), a, s);
-            if (e != hipSuccess) return e;
-        }
-        return hipSuccess;
-    });
-    note_stream(p, s);
+    rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, dst, s);
+    if (rc == FC_OK) {
+        fc::BcastArgs a{};
+        a.tiles = p->d_tiles;
+        a.ntiles = p->ntiles;
+        a.src = src;
+        a.dst = p->d_dst;
+        a.K = p->K;
+        rc = launch(p, FC_KERNEL_BCAST, s, [&] {
+            if (p->schedule != FC_SCHED_RESIDENT) return fc::launch_bcast(p->shape, p->grid, a, s);
+            // resident plans: the step's ranges, one launch per round
+            for (int round = 0; round < p->res_rounds; ++round) {
+                a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
+                const hipError_t e =
+                    fc::launch_resident_bcast(p->shape, p->res_grid, static_cast<size_t>(p->res_lds), a, s);
+                if (e != hipSuccess) return e;
+            }
+            return hipSuccess;
+        });
+    }
+    if (note) note_stream(p, s);
     return rc;
 }
 
-static int fc_step_body(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
-            float* out, float* const* bcast_dst, void* stream) {
+namespace {
+
+// What fc_step checks before it enqueues anything.
+int check_step(const fc_plan* p, const void* const* grads, float* w, float* v, int batch, float* out,
+               float* const* bcast_dst) {
     if (!p || !w || !v || batch < 1) return FC_EINVAL;
     if (!aligned16(w) || !aligned16(v) || (out && !aligned16(out))) return FC_EALIGN;
-    std::vector<Span> spans;
+    Spans spans;
     int rc = check_replicas(p, grads, spans);
     if (rc) return rc;
-    spans.push_back(span_of(p, w, 4, true, ID_W, false));
-    spans.push_back(span_of(p, v, 4, true, ID_V, false));
-    if (out) spans.push_back(span_of(p, out, 4, true, ID_OUT, false));
+    spans.push(span_of(p, w, 4, true, ID_W, false));
+    spans.push(span_of(p, v, 4, true, ID_V, false));
+    if (out) spans.push(span_of(p, out, 4, true, ID_OUT, false));
     if (bcast_dst) {
         rc = check_dsts(p, bcast_dst, spans);
         if (rc) return rc;
     }
-    rc = check_aliasing(spans, out ? ID_OUT : -1, p->gdt == FC_F32);
+    return check_aliasing(spans, out ? ID_OUT : -1, p->gdt == FC_F32);
+}
+
+// The replica table, and the destination table when broadcasting.
+int update_step_tables(fc_plan* p, const void* const* grads, float* const* bcast_dst, hipStream_t s) {
+    int rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    if (rc == FC_OK && bcast_dst) rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, bcast_dst, s);
+    return rc;
+}
+
+// Two passes on the plan's tiles: the reduce kernel stores the raw sum into
+// `sum`, then the SGD kernel updates w, v from it (and stores the broadcast
+// copies).  `sh` is the launch shape of both passes.
+int two_pass(fc_plan* p, const fc::Shape& sh, float* sum, float* w, float* v, float lr, float mu, float wd,
+             float c, bool bcast, hipStream_t s, bool timed) {
+    fc::ReduceArgs r{};
+    r.tiles = p->d_tiles;
+    r.ntiles = p->ntiles;
+    r.mults = p->d_mults;
+    r.grads = p->d_grads;
+    r.K = p->K;
+    r.out = sum;
+    fc::SgdArgs g{};
+    g.tiles = p->d_tiles;
+    g.ntiles = p->ntiles;
+    g.mults = p->d_mults;
+    g.w = w;
+    g.v = v;
+    g.g = sum;
+    g.dst = bcast ? p->d_dst : nullptr;
+    g.K = p->K;
+    g.lr = lr;
+    g.mu = mu;
+    g.wd = wd;
+    g.c = c;
+    if (!timed) {
+        int rc = hip_rc(launch_reduce(sh, fc::MODE_REDUCE, p->grid, r, s));
+        return rc ? rc : hip_rc(fc::launch_sgd(sh, p->grid, g, s));
+    }
+    int rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(sh, fc::MODE_REDUCE, p->grid, r, s); });
+    if (rc == FC_OK) rc = launch(p, FC_KERNEL_SGD, s, [&] { return fc::launch_sgd(sh, p->grid, g, s); });
+    return rc;
+}
+
+}  // namespace
+
+static int fc_step_body(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
+            float* out, float* const* bcast_dst, void* stream) {
+    int rc = check_step(p, grads, w, v, batch, out, bcast_dst);
     if (rc) return rc;
     if (p->ntiles == 0) return FC_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = update_table<const void*>(p, p->h_grads, p->grads_valid, p->d_grads, grads, s);
+    bool note = false;
+    rc = order_after_last(p, s, note);
     if (rc) return rc;
-    if (bcast_dst) {
-        rc = update_table<float*>(p, p->h_dst, p->dst_valid, p->d_dst, bcast_dst, s);
-        if (rc) return rc;
-    }
+    rc = update_step_tables(p, grads, bcast_dst, s);
     const float c = 1.0f / static_cast<float>(batch);
-    if (p->schedule == FC_SCHED_TWO_PASS) {
+    if (rc == FC_OK && p->schedule == FC_SCHED_TWO_PASS) {
         // pass 1: raw sum into `out` (or the plan's scratch); pass 2: update (+ broadcast)
-        float* sum = out ? out : p->d_sum;
-        fc::ReduceArgs r{};
-        r.tiles = p->d_tiles;
-        r.ntiles = p->ntiles;
-        r.mults = p->d_mults;
-        r.grads = p->d_grads;
-        r.K = p->K;
-        r.span = p->shape.span;
-        r.out = sum;
-        rc = launch(p, FC_KERNEL_REDUCE, s, [&] { return launch_reduce(p->shape, fc::MODE_REDUCE, p->grid, r, s); });
-        if (rc == FC_OK) {
-            fc::SgdArgs g{};
-            g.tiles = p->d_tiles;
-            g.ntiles = p->ntiles;
-            g.mults = p->d_mults;
-            g.w = w;
-            g.v = v;
-            g.g = sum;
-            g.dst = bcast_dst ? p->d_dst : nullptr;
-            g.K = p->K;
-            g.lr = lr;
-            g.mu = mu;
-            g.wd = wd;
-            g.c = c;
-            rc = launch(p, FC_KERNEL_SGD, s, [&] { return fc::launch_sgd(p->shape, p->grid, g, s); });
-        }
-        note_stream(p, s);
-        return rc;
+        rc = two_pass(p, p->shape, out ? out : p->d_sum, w, v, lr, mu, wd, c, bcast_dst != nullptr, s, true);
+    } else if (rc == FC_OK) {
+        fc::ReduceArgs a{};
+        a.tiles = p->d_tiles;
+        a.ntiles = p->ntiles;
+        a.mults = p->d_mults;
+        a.grads = p->d_grads;
+        a.K = p->K;
+        a.w = w;
+        a.v = v;
+        a.out = out;
+        a.dst = bcast_dst ? p->d_dst : nullptr;
+        a.lr = lr;
+        a.mu = mu;
+        a.wd = wd;
+        a.c = c;
+        rc = launch(p, FC_KERNEL_STEP, s, [&] {
+            return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_STEP, a, s)
+                                                    : launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s);
+        });
     }
-    fc::ReduceArgs a{};
-    a.tiles = p->d_tiles;
-    a.ntiles = p->ntiles;
-    a.mults = p->d_mults;
-    a.grads = p->d_grads;
-    a.K = p->K;
-    a.span = p->shape.span;
-    a.w = w;
-    a.v = v;
-    a.out = out;
-    a.dst = bcast_dst ? p->d_dst : nullptr;
-    a.lr = lr;
-    a.mu = mu;
-    a.wd = wd;
-    a.c = c;
-    rc = launch(p, FC_KERNEL_STEP, s, [&] {
-        return p->schedule == FC_SCHED_RESIDENT ? launch_resident(p, fc::MODE_STEP, a, s)
-                                                : launch_reduce(p->shape, fc::MODE_STEP, p->grid, a, s);
-    });
-    note_stream(p, s);
+    if (note) note_stream(p, s);
     return rc;
 }
 

@@ -31,8 +31,6 @@
 // Kernels (all share the loads, the register stack and the epilogue, so they
 // give the same bits):
 //   reduce_kernel   one tile per block; reduce-only, or the fused step
-//   ksplit_kernel   the K replicas split over the waves of a block, combined
-//                   in tree order through LDS
 //   resident_kernel one persistent block per CU: reduce a range of tiles into
 //                   LDS (pure reads), then finish it from LDS (and store the
 //                   broadcast copies one destination at a time)
@@ -507,108 +505,6 @@ __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uin
     }
 }
 
-// ------------------------------------------------------------------ K split across waves
-// A block of W waves shares one tile of 64*U lane-vectors.  The K leaves are
-// cut into aligned runs of S = a.span leaves (a power of two, a multiple of
-// C): wave q < nq = K / S reduces run q, which is a complete subtree of the
-// reduction tree; when K is not a multiple of S, wave nq reduces the r = K -
-// nq*S leaves left over, folding its pending subtrees newest first exactly as
-// reduce() does.  Those subtrees are all smaller than S, so over the whole
-// counter they never merge with a run: the binary counter over K leaves is the
-// counter over the nq run sums, folded onto the left-over value as the newest
-// term.  The partial sums meet in LDS, where one thread per lane-vector
-// finishes the tree that way.  Each wave streams 64*U contiguous vectors of
-// each of its replicas (4 KiB of fp32 for U = 4) while holding a stack for
-// only S leaves.
-template <int DT, int W, int V, int U, int C, int D, int MODE>
-__device__ __forceinline__ void ksplit_body(const ReduceArgs& a, float* part, uint64_t start, uint32_t count,
-                                            float lr_j, float wd_j) {
-    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
-    constexpr int WAVE = 64;
-    constexpr int DC = ilog2<W>() + 1;  // counter over at most W runs
-    const int lane = threadIdx.x & (WAVE - 1);
-    const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
-    const int S = a.span;
-    const int nq = a.K / S;
-    const int r = a.K - nq * S;
-    if (q < nq || (q == nq && r)) {
-        uint32_t roff[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t vi = lane + u * WAVE;
-            roff[u] = (vi < count ? vi : 0u) * V * SG;  // idle lanes re-read vector 0
-        }
-        Acc<U, V> x;
-        reduce<DT, V, U, C, D, true>(a.grads + q * S, q < nq ? S : r, start * SG, roff, x);
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int i = 0; i < V; ++i) part[((q * U + u) * WAVE + lane) * V + i] = x.a[u][i];
-    }
-    __syncthreads();
-    const uint64_t start4 = start * 4;
-    for (int e = threadIdx.x; e < U * WAVE; e += W * WAVE) {
-        // tile vector e = lane e % 64, vector e / 64: its partials sit at (q*U*64 + e)*V
-        Acc<1, V> acc;
-        if (nq == W && !r) {
-            // K = W * S: the W runs are the leaves of one balanced subtree.  The
-            // counter with constant indices has no selects (the combine's
-            // latency is exposed to the whole block) and holds log2(W) + 1
-            // partials instead of W.
-            Acc<1, V> st[DC];
-#pragma unroll
-            for (int n = 0; n < W; ++n) {
-                Acc<1, V> p;
-#pragma unroll
-                for (int i = 0; i < V; ++i) p.a[0][i] = part[(n * U * WAVE + e) * V + i];
-                push<DC>(st, p, n);
-            }
-            set(acc, st[DC - 1]);
-        } else {
-            Acc<1, V> st[DC];
-            bool have = false;
-            if (r) {
-#pragma unroll
-                for (int i = 0; i < V; ++i) acc.a[0][i] = part[(nq * U * WAVE + e) * V + i];
-                have = true;
-            }
-            for (int n = 0; n < nq; ++n) {
-                Acc<1, V> p;
-#pragma unroll
-                for (int i = 0; i < V; ++i) p.a[0][i] = part[(n * U * WAVE + e) * V + i];
-                push<DC>(st, p, n);
-            }
-            fold<DC>(st, nq, acc, have);
-        }
-        if (static_cast<uint32_t>(e) >= count) continue;
-        finish<V, MODE>(a, start4, static_cast<uint32_t>(e) * V * 4, acc.a[0], lr_j, wd_j);
-    }
-    __syncthreads();  // the partials are overwritten by the block's next tile
-}
-
-// D: depth of each wave's pending-subtree stack (>= bit length of span / C).
-// The reduce-only kernel with U = 2 and C = 2 is held to 64 registers (8
-// waves per SIMD), so that two blocks of 16 waves share a CU and one block's
-// combine overlaps the other's loads (the fused variant would spill).
-template <int DT, int W, int U, int C, int D, int MODE>
-__global__ __launch_bounds__(64 * W, (U == 2 && C == 2 && MODE == MODE_REDUCE) ? 8 : 1) void ksplit_kernel(
-    ReduceArgs a) {
-    __shared__ __attribute__((aligned(16))) float part[W * U * 64 * 4];
-    for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
-        const Tile tile = ld_tile(a.tiles, t);
-        float lr_j = 0.0f, wd_j = 0.0f;
-        if constexpr (MODE == MODE_STEP) {
-            const int j = static_cast<int>(tile.seg & SEG_MASK);
-            lr_j = a.lr * ldc(a.mults, 2 * j);
-            wd_j = a.wd * ldc(a.mults, 2 * j + 1);
-        }
-        if (!(tile.seg & TAIL_BIT))
-            ksplit_body<DT, W, 4, U, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
-        else
-            ksplit_body<DT, W, 1, 1, C, D, MODE>(a, part, tile.start, tile.count, lr_j, wd_j);
-    }
-}
-
 // The broadcast phase of the resident kernels: the values of the block's
 // tiles [lo, hi) sit in their LDS slots (tile lo + j in slot j, parked there
 // by wave j mod W), and the block stores them to the K destinations one
@@ -892,34 +788,8 @@ hipError_t go_reduce(int grid, int block, const ReduceArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-// (waves, lane vectors, replicas per batch) triples compiled for the K split,
-// each with a stack deep enough for runs of up to 8 batches.
-template <class F> hipError_t pick_ksplit(int w, int u, int c, F&& f) {
-    constexpr int D = KSPLIT_MAXD;
-    if (u == 4 && c == 2) {
-        if (w == 4) return f(I<4>{}, I<4>{}, I<2>{}, I<D>{});
-        if (w == 8) return f(I<8>{}, I<4>{}, I<2>{}, I<D>{});
-        if (w == 16) return f(I<16>{}, I<4>{}, I<2>{}, I<D>{});
-    }
-    if (u == 2 && c == 4) {
-        if (w == 8) return f(I<8>{}, I<2>{}, I<4>{}, I<D>{});
-        if (w == 16) return f(I<16>{}, I<2>{}, I<4>{}, I<D>{});
-    }
-    if (u == 2 && c == 2 && w == 16) return f(I<16>{}, I<2>{}, I<2>{}, I<D>{});
-    return hipErrorInvalidValue;
-}
-
 template <int DT>
 hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s) {
-    if (sh.kwaves > 1) {
-        return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
-            return pick_ksplit(sh.kwaves, sh.vecs, sh.kchunk, [&](auto w, auto u, auto c, auto d) {
-                hipLaunchKernelGGL((ksplit_kernel<DT, w.value, u.value, c.value, d.value, md.value>), dim3(grid),
-                                   dim3(64 * w.value), 0, s, a);
-                return hipGetLastError();
-            });
-        });
-    }
     return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
         return pick_uc(sh.vecs, sh.kchunk, [&](auto u, auto c) {
             if (sh.tree) {

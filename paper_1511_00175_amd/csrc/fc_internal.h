@@ -33,9 +33,6 @@ struct Shape {
     int vecs;         // 4-element lane-vectors per thread (1, 2 or 4)
     int kchunk;       // replicas loaded per batch (2, 4, 8 or 16; see the pairs compiled)
     int maxd;         // depth of the pending-subtree stack (>= bit length of K / kchunk)
-    int kwaves;       // waves of a reduce block that split the K replicas (1: no split)
-    int span;         // with kwaves > 1: replicas per wave, a power of two multiple of kchunk
-    int lanes;        // lanes per tile: block, or 64 when the K replicas are split
 };
 
 struct ReduceArgs {
@@ -44,7 +41,6 @@ struct ReduceArgs {
     const float* mults;           // per segment j: lr_mult at 2j, decay_mult at 2j+1
     const void* const* grads;     // device table of K replica pointers
     int K;
-    int span;                     // replicas per wave when the K replicas are split
     float* w;
     float* v;
     float* out;                   // raw sum or nullptr
@@ -96,12 +92,6 @@ struct BcastArgs {
 // Largest pending-subtree stack depth compiled (stack depths 5, 7 and 10 are
 // instantiated); plans whose K / kchunk needs more are rejected at creation.
 constexpr int MAXD_MAX = 10;
-
-// K split across the waves of a block: the deepest per-wave stack compiled.
-// A wave's run of `span` replicas takes at most KSPLIT_MAX_BATCHES batches of
-// kchunk.
-constexpr int KSPLIT_MAXD = 4;
-constexpr int KSPLIT_MAX_BATCHES = 8;
 
 hipError_t launch_reduce_f32(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);
 hipError_t launch_reduce_f16(const Shape& sh, int mode, int grid, const ReduceArgs& a, hipStream_t s);

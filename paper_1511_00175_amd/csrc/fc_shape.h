@@ -18,18 +18,6 @@ namespace fc {
 // Four vectors per lane make every wave read 4 KiB of one replica at a time,
 // which HBM serves better than 1 KiB pieces, as long as the lane's registers
 // (16 accumulators per pending subtree) still allow enough waves in flight.
-// K split across waves by default in the fused and two-pass schedules (8
-// waves, 4 vectors per lane, 2 replicas per batch) for fp32 replicas in tree
-// order with 16 <= K <= 48
-// when w and v (8 bytes per parameter) exceed the 256 MiB Infinity Cache:
-// measured on MI355X, VGG-19-sized plans gain 5-12% at K = 16..32 and
-// AlexNet-sized fp32 plans 2-4%, while plans whose w, v stay cache-resident
-// (NiN, GoogLeNet) gain nothing and small K (<= 12) or K = 64 lose.
-inline int default_kwaves(fc_dtype gdt, fc_order order, int K, uint64_t n_elems) {
-    const bool big = n_elems >= (uint64_t(1) << 25);
-    return gdt == FC_F32 && order == FC_ORDER_TREE && K >= 16 && K <= 48 && big ? 8 : 1;
-}
-
 inline void default_shape(fc_dtype gdt, int K, fc::Shape& sh) {
     if (gdt == FC_F16) {
         sh.vecs = 4; sh.kchunk = 4; sh.block = 256;
@@ -38,21 +26,6 @@ inline void default_shape(fc_dtype gdt, int K, fc::Shape& sh) {
     } else {
         sh.vecs = 1; sh.kchunk = 16; sh.block = 64;
     }
-}
-
-// K split across the waves of a block (tree order only): the compiled
-// (waves, lane vectors, replicas per batch) triples.
-inline bool compiled_ksplit(int w, int u, int c) {
-    return (u == 4 && c == 2 && (w == 4 || w == 8 || w == 16)) || (u == 2 && c == 4 && (w == 8 || w == 16)) ||
-           (u == 2 && c == 2 && w == 16);
-}
-
-// Replicas per wave for a K split over w waves: the smallest power of two
-// that is at least kchunk and covers K in w runs.
-inline int ksplit_span(int K, int w, int c) {
-    int s = c;
-    while (static_cast<int64_t>(s) * w < K) s *= 2;
-    return s;
 }
 
 // (lane vectors, replicas per batch) of the resident kernel's tiles; with

@@ -5,9 +5,10 @@
 
 namespace fc {
 
+
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s) {
     auto go = [&](auto u) {
-        hipLaunchKernelGGL((sgd_kernel<4, u.value>), dim3(grid), dim3(sh.lanes), 0, s, a);
+        hipLaunchKernelGGL((sgd_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
         return hipGetLastError();
     };
     if (sh.vecs == 4) return go(I<4>{});
@@ -16,7 +17,7 @@ hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s
 
 hipError_t launch_bcast(const Shape& sh, int grid, const BcastArgs& a, hipStream_t s) {
     auto go = [&](auto u) {
-        hipLaunchKernelGGL((bcast_kernel<4, u.value>), dim3(grid), dim3(sh.lanes), 0, s, a);
+        hipLaunchKernelGGL((bcast_kernel<4, u.value>), dim3(grid), dim3(sh.block), 0, s, a);
         return hipGetLastError();
     };
     if (sh.vecs == 4) return go(I<4>{});

@@ -72,19 +72,12 @@ def test_plan_argument_errors(fcmod, segs, K, gdt, opts, code):
 
 
 @pytest.mark.parametrize("K,order,opts", [
-    (8, 1, {"k_waves": 4}),                             # split needs the tree order
-    (65, 0, {"k_waves": 4}),                            # a run would take more than 8 batches
-    (257, 0, {"k_waves": 16}),
-    (257, 0, {"k_waves": 8, "vecs_per_thread": 2, "kchunk": 4}),
-    (8, 0, {"k_waves": 8, "vecs_per_thread": 2, "kchunk": 2}),  # triple not compiled
-    (8, 0, {"k_waves": 2}),                             # waves not compiled
-    (8, 0, {"k_waves": 32}),
+    (8, 0, {"k_waves": 2}),                             # one wave per lane-vector only
+    (8, 1, {"k_waves": 4}),
+    (128, 0, {"k_waves": 16}),
     (8, 0, {"k_waves": -1}),
-    (8, 0, {"k_waves": 4, "block_threads": 256 + 64}),  # block must be 64 * waves
-    (8, 0, {"k_waves": 4, "kchunk": 4}),                # triple not compiled
-    (8, 0, {"k_waves": 4, "vecs_per_thread": 1}),
 ])
-def test_ksplit_option_errors(fcmod, K, order, opts):
+def test_k_waves_errors(fcmod, K, order, opts):
     rc, h = fcmod._fc.fc_plan_create([(0, 16)], K, 0, order, opts)
     assert rc == fcmod._fc.FC_EINVAL and not h.value
 
@@ -122,8 +115,7 @@ def test_oracle_and_library_share_nothing():
 def test_kernels_use_no_scratch_memory():
     """The build records the compiler's per-kernel resource usage: every
     kernel keeps its pending-subtree stack and partial sums in registers and
-    LDS (no scratch memory), and the K-split kernels' LDS fits two blocks per
-    CU where it is meant to."""
+    LDS (no scratch memory)."""
     path = os.path.join(ROOT, "paper_1511_00175_amd", "_build", "kernel_resources.txt")
     if not os.path.exists(path):
         pytest.skip("library not built by paper_1511_00175_amd/build.py")
@@ -134,8 +126,7 @@ def test_kernels_use_no_scratch_memory():
             rows[name] = dict(x.split("=") for x in kv)
     assert len(rows) >= 100
     assert all(r["ScratchSize"] == "0" for r in rows.values())
-    ks = [n for n in rows if "ksplit_kernel" in n]
-    assert ks and all(int(rows[n]["LDS"]) <= 65536 for n in ks)
+    assert any("resident_kernel" in n for n in rows) and any("reduce_kernel" in n for n in rows)
 
 
 def test_read_probe_argument_errors(fcmod):

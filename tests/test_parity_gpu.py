@@ -103,7 +103,6 @@ def test_fp16_widening_exhaustive(fc):
 PAIRS = [(1, 8), (1, 16), (2, 8), (2, 16), (4, 2), (4, 4), (4, 8)]
 SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c) for b in (64, 128, 256) for u, c in PAIRS]
 SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, kchunk=8, max_blocks=5)]
-SHAPES += [dict(k_waves=8), dict(k_waves=16), dict(k_waves=16, schedule=2), dict(k_waves=8, max_blocks=3)]
 SHAPES += [dict(schedule=3), dict(schedule=3, max_blocks=7), dict(schedule=3, max_blocks=1)]
 
 
@@ -121,72 +120,6 @@ def test_launch_shape_invariance(fc, dtype):
             ref = got
         assert same_bits(got, ref) == 0
         assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(6), steps=1, opts=opts) == 0, opts
-
-
-# (waves, lane vectors, batch, K): complete runs only, a left-over run, idle
-# waves, runs of one batch and of the most batches a wave may take (8).
-KSPLIT = [(4, 4, 2, K) for K in (1, 2, 3, 5, 8, 13, 31, 32, 64)] + \
-         [(8, 4, 2, K) for K in (7, 16, 33, 100, 128)] + \
-         [(16, 4, 2, K) for K in (17, 100, 127, 128, 255, 256)] + \
-         [(8, 2, 4, K) for K in (4, 9, 64, 129, 256)] + \
-         [(16, 2, 4, K) for K in (16, 65, 128, 512)] + \
-         [(16, 2, 2, K) for K in (1, 40, 128)]
-
-
-@pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("kw,u,c,K", KSPLIT)
-def test_ksplit_matches_oracle(fc, kw, u, c, K, dtype):
-    """K split across the waves of a block: aligned runs of replicas reduced
-    by separate waves, then combined through LDS, give the oracle's tree bits
-    in the reduce and in both step schedules (with raw sum and broadcast)."""
-    segs = table(11000 + K, dtype, nseg=6, max_len=4000 if K <= 128 else 1500)
-    rng = np.random.default_rng(K * 7 + kw)
-    opts = dict(k_waves=kw, vecs_per_thread=u, kchunk=c)
-    bad, _, _ = run_reduce(fc, segs, K, dtype, "tree", rng, opts=opts)
-    assert bad == 0
-    for schedule in (1, 2):
-        assert run_steps(fc, segs, K, dtype, "tree", rng, steps=2, opts=dict(opts, schedule=schedule),
-                         with_out=True, with_bcast=K <= 16) == 0, schedule
-
-
-@pytest.mark.parametrize("K", [5, 33, 128])
-def test_ksplit_special_values(fc, K):
-    segs = table(12000 + K, "f32", nseg=4, max_len=2000)
-    for dtype in ("f32", "f16"):
-        bad, _, _ = run_reduce(fc, segs, K, dtype, "tree", np.random.default_rng(K), opts=dict(k_waves=16),
-                               special=True)
-        assert bad == 0, dtype
-
-
-def test_ksplit_plan_info(fc):
-    segs = [(0, 5000, 1, 1), (5120, 7, 1, 1)]
-    p = fc.Plan(segs, 100, "f32", "tree", k_waves=16)
-    info = p.info()
-    assert (info.k_waves, info.block_threads, info.vecs_per_thread, info.kchunk) == (16, 1024, 4, 2)
-    # tiles of 64 lanes x 4 vectors: ceil(1250 / 256) + ceil(1 / 256) + one tail tile
-    assert info.ntiles == 5 + 1 + 1
-    p.close()
-    p = fc.Plan(segs, 100, "f32", "tree", block_threads=64)
-    assert p.info().k_waves == 1
-    p.close()
-
-
-def test_ksplit_default_rule(fc):
-    """In the fused schedule the split is the default only for fp32 tree
-    plans with 16 <= K <= 48 and at least 2^25 parameters (without a schedule
-    such plans are resident)."""
-    big = [(0, 1 << 25, 1, 1)]
-    small = [(0, (1 << 25) - 4, 1, 1)]
-    for segs, K, dtype, order, kw in ((big, 16, "f32", "tree", 8), (big, 48, "f32", "tree", 8),
-                                      (big, 15, "f32", "tree", 1), (big, 49, "f32", "tree", 1),
-                                      (big, 16, "f32", "linear", 1), (big, 16, "f16", "tree", 1),
-                                      (small, 16, "f32", "tree", 1)):
-        p = fc.Plan(segs, K, dtype, order, schedule=1)
-        assert p.info().k_waves == kw, (K, dtype, order, len(segs))
-        p.close()
-    p = fc.Plan(big, 16, "f32", "tree")
-    assert (p.info().schedule, p.info().k_waves) == (3, 1)
-    p.close()
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
@@ -915,3 +848,38 @@ def test_balance_with_full_lds_keeps_equal_shares(fc):
                     after_step=lambda plan: rates.append(plan.balance()))
     assert bad == 0
     assert sum(1 for r in rates[-1] if r > 0) == 2
+
+
+@pytest.mark.parametrize("schedule", [2, 3])
+def test_calls_on_several_streams_are_ordered(fc, schedule):
+    """Steps of one plan on three streams, each on its own w, v, with the
+    replica table replaced between them: every call runs after the plan's
+    previous call whatever its stream, so a table replaced for a later call
+    is never read by an earlier one still running, and the two-pass raw-sum
+    scratch never serves two calls at once.  Every result equals the
+    oracle's, applied in the order of the calls."""
+    import torch
+    K = 70
+    segs = [(0, 1 << 21, 1.0, 1.0), ((1 << 21) + 64, 1000, 1.0, 1.0)]
+    n = alloc_len(segs)
+    rng = np.random.default_rng(77)
+    sets_h = [host_replicas(rng, K, n, np.float32, scale=0.01) for _ in range(2)]
+    sets = [to_dev(r) for r in sets_h]
+    ws_h = [rng.standard_normal(n, dtype=np.float32) * np.float32(0.05) for _ in range(4)]
+    vs_h = [np.zeros(n, np.float32) for _ in range(4)]
+    ws, vs = [to_dev(w) for w in ws_h], [to_dev(v) for v in vs_h]
+    p = fc.Plan(segs, K, "f32", "tree", schedule=schedule)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    for st in streams:
+        st.wait_stream(torch.cuda.current_stream())
+    # (stream, replica set, w/v set)
+    calls = [(0, 0, 0), (1, 0, 1), (2, 1, 2), (0, 0, 3), (1, 1, 0), (2, 1, 1), (0, 0, 2)]
+    for si, r, j in calls:
+        with torch.cuda.stream(streams[si]):
+            p.step(sets[r], ws[j], vs[j], LR, MU, WD, 256)
+        ws_h[j], vs_h[j], _, _ = oracle.step(segs, list(sets_h[r]), ws_h[j], vs_h[j], LR, MU, WD, 256)
+    torch.cuda.synchronize()
+    p.close()
+    for j in range(4):
+        assert same_bits(ws[j].cpu().numpy(), ws_h[j]) == 0, j
+        assert same_bits(vs[j].cpu().numpy(), vs_h[j]) == 0, j
