@@ -72,6 +72,7 @@ extern "C" {
 #define FC_EALIAS (-3) /* a written buffer overlaps another buffer (see each call) */
 #define FC_EHIP (-4)   /* the HIP runtime reported an error (allocation, copy or launch) */
 #define FC_ENOMEM (-5) /* host allocation failed */
+#define FC_ESIZE (-6)  /* fc_step_noalloc: the plan is larger than its fixed raw-sum array */
 
 /* One segment = one layer's weight or bias block (Sec. 3, Eq. 1).  Offsets and
  * lengths are in elements.  Segments must be sorted by offset and must not
@@ -207,6 +208,28 @@ int fc_broadcast(fc_plan* plan, const float* src, float* const* dst, void* strea
  * (FC_EALIAS), except out == grads[k] as above. */
 int fc_step(fc_plan* plan, const void* const* grads, float* w, float* v, float lr, float mu,
             float wd, int batch, float* out, float* const* bcast_dst, void* stream);
+
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: fc_step in
+ * the two-pass schedule (a reduce pass into a raw-sum buffer, then the update
+ * pass, which also stores the broadcast copies), whatever the plan's own
+ * schedule, with the raw sum between the passes held in a fixed device array
+ * of FC_NOALLOC_MAX_ELEMS floats (64 MiB) that the library reserves on each
+ * GPU it runs on and keeps until the process ends.  Arguments, validation
+ * and result bits are fc_step's.  When `out` is given it holds the raw sum
+ * between the passes and the array is not used; otherwise the plan's extent
+ * (one past its last segment element) must be at most FC_NOALLOC_MAX_ELEMS
+ * (FC_ESIZE).  The current device must be the plan's (FC_EINVAL).  The call
+ * allocates no device or host memory and records no per-kernel timing; like
+ * every call it replaces a pointer table only when the pointers change.
+ * Every call on one GPU uses that GPU's one array: calls that may run at the
+ * same time on one GPU (other plans, other streams or threads) race on it;
+ * calls on one plan are ordered (see the conventions above).  The array
+ * needs no clearing: the reduce pass writes every segment element before the
+ * update pass reads it. */
+#define FC_NOALLOC_MAX_ELEMS 16777216
+int fc_step_noalloc(fc_plan* plan, const void* const* grads, float* w, float* v, float lr, float mu,
+                    float wd, int batch, float* out, float* const* bcast_dst, void* stream);
 
 /* Learning-rate policies (Sec. 7.2 "Results: Midsized deep models", Sec. 7.3
  * "Results: Ultra-deep models").  The rate at iteration `iter` for a step of

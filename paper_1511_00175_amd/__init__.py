@@ -9,14 +9,15 @@ The work is done by HIP kernels behind the C ABI of include/fc.h; this package
 only marshals torch tensors (device memory and the current stream) into it.
 """
 from . import _fc
-from ._fc import (FC_F16, FC_F32, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO,  # noqa: F401
+from ._fc import (FC_F16, FC_F32, FC_NOALLOC_MAX_ELEMS, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO,  # noqa: F401
                   FC_SCHED_FUSED, FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create,
                   fc_plan_destroy, fc_plan_query, fc_lr_at, fc_plan_balance, fc_plan_read_timing, fc_plan_set_timing,
-                  fc_read_probe, fc_read_probe_blocks, fc_sgd_step, fc_step, fc_strerror, fc_train,
+                  fc_read_probe, fc_read_probe_blocks, fc_sgd_step, fc_step, fc_step_noalloc, fc_strerror, fc_train,
                   fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
-           "fc_plan_read_timing", "fc_plan_balance", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step", "fc_strerror",
+           "fc_plan_read_timing", "fc_plan_balance", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
+           "fc_step_noalloc", "fc_strerror",
            "fc_lr_at", "fc_train", "lr_policy", "lr_at", "fc_read_probe", "fc_read_probe_blocks", "read_probe"]
 
 
@@ -209,3 +210,10 @@ class Plan:
         if rc:
             raise FcError("fc_step", rc)
 
+    def step_noalloc(self, grads, w, v, lr, mu, wd, batch, out=None, bcast=None, stream=None):
+        """fc_step_noalloc: the step in two passes with the raw sum in the
+        library's fixed device array (no allocation)."""
+        g, wp, vp, op, bp = self._step_args(grads, w, v, out, bcast)
+        rc = fc_step_noalloc(self.handle, g, wp, vp, lr, mu, wd, batch, op, bp, _stream(stream))
+        if rc:
+            raise FcError("fc_step_noalloc", rc)

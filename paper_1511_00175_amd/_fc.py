@@ -11,7 +11,8 @@ import os
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("FC_LIBRARY", os.path.join(PKG, "libfc.so"))
 
-FC_OK, FC_EINVAL, FC_EALIGN, FC_EALIAS, FC_EHIP, FC_ENOMEM = 0, -1, -2, -3, -4, -5
+FC_OK, FC_EINVAL, FC_EALIGN, FC_EALIAS, FC_EHIP, FC_ENOMEM, FC_ESIZE = 0, -1, -2, -3, -4, -5, -6
+FC_NOALLOC_MAX_ELEMS = 16777216  # floats in the fixed raw-sum array of fc_step_noalloc
 FC_F32, FC_F16 = 0, 1
 FC_ORDER_TREE, FC_ORDER_LINEAR = 0, 1
 
@@ -73,6 +74,7 @@ lib.fc_tree_reduce.argtypes = [_plan_p, _pp, _vp, _vp]
 lib.fc_sgd_step.argtypes = [_plan_p, _vp, _vp, _vp, _f, _f, _f, _i, _vp]
 lib.fc_broadcast.argtypes = [_plan_p, _vp, _pp, _vp]
 lib.fc_step.argtypes = [_plan_p, _pp, _vp, _vp, _f, _f, _f, _i, _vp, _pp, _vp]
+lib.fc_step_noalloc.argtypes = [_plan_p, _pp, _vp, _vp, _f, _f, _f, _i, _vp, _pp, _vp]
 lib.fc_strerror.argtypes = [_i]
 lib.fc_strerror.restype = ctypes.c_char_p
 lib.fc_plan_query.argtypes = [_plan_p, ctypes.POINTER(fc_plan_info)]
@@ -86,6 +88,7 @@ lib.fc_plan_set_timing.argtypes = [_plan_p, _i]
 lib.fc_plan_read_timing.argtypes = [_plan_p, ctypes.POINTER(fc_timing)]
 lib.fc_plan_balance.argtypes = [_plan_p, _vp, ctypes.POINTER(ctypes.c_float), _i]
 for _n in ("fc_plan_create", "fc_plan_create_ex", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
+           "fc_step_noalloc",
            "fc_plan_query", "fc_plan_set_timing", "fc_plan_read_timing", "fc_lr_at", "fc_train",
            "fc_read_probe", "fc_plan_balance"):
     getattr(lib, _n).restype = ctypes.c_int
@@ -183,6 +186,11 @@ def fc_broadcast(plan, src, dst, stream=0):
 
 def fc_step(plan, grads, w, v, lr, mu, wd, batch, out=None, bcast_dst=None, stream=0):
     return lib.fc_step(plan, _ptr_array(grads), w, v, lr, mu, wd, int(batch), out, _ptr_array(bcast_dst), stream)
+
+
+def fc_step_noalloc(plan, grads, w, v, lr, mu, wd, batch, out=None, bcast_dst=None, stream=0):
+    return lib.fc_step_noalloc(plan, _ptr_array(grads), w, v, lr, mu, wd, int(batch), out, _ptr_array(bcast_dst),
+                               stream)
 
 
 _LR_KINDS = {"fixed": FC_LR_FIXED, "step": FC_LR_STEP, "poly": FC_LR_POLY}

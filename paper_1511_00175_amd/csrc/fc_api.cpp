@@ -347,6 +347,7 @@ const char* fc_strerror(int code) {
         case FC_EALIAS: return "a written buffer overlaps another buffer";
         case FC_EHIP: return "HIP runtime error";
         case FC_ENOMEM: return "out of host memory";
+        case FC_ESIZE: return "plan larger than the fixed raw-sum array of fc_step_noalloc";
         default: return "unknown error code";
     }
 }
@@ -798,7 +799,7 @@ static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, vo
 
 namespace {
 
-// What fc_step checks before it enqueues anything.
+// What fc_step and fc_step_noalloc check before they enqueue anything.
 int check_step(const fc_plan* p, const void* const* grads, float* w, float* v, int batch, float* out,
                float* const* bcast_dst) {
     if (!p || !w || !v || batch < 1) return FC_EINVAL;
@@ -897,6 +898,44 @@ static int fc_step_body(fc_plan* p, const void* const* grads, float* w, float* v
     return rc;
 }
 
+// fc_step's two-pass schedule with the raw sum in the library's fixed device
+// array (fc_update.hip) instead of memory the plan owns; it allocates
+// nothing, on the device or on the host.
+static int fc_step_noalloc_body(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu,
+                                float wd, int batch, float* out, float* const* bcast_dst, void* stream) {
+    int rc = check_step(p, grads, w, v, batch, out, bcast_dst);
+    if (rc) return rc;
+    if (!out && p->extent > static_cast<uint64_t>(FC_NOALLOC_MAX_ELEMS)) return FC_ESIZE;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return FC_EHIP;
+    if (dev != p->device) return FC_EINVAL;
+    if (p->ntiles == 0) return FC_OK;
+    // both passes run on the plan's tiles (block * vecs lane-vectors each);
+    // a resident plan's batch of 4 replicas has no reduce-kernel instance,
+    // so its reduce pass loads batches of 8 (the association does not depend
+    // on the batch)
+    fc::Shape sh = p->shape;
+    if (!fc::compiled_pair(sh.vecs, sh.kchunk)) {
+        sh.kchunk = 8;
+        sh.maxd = bit_length(p->K / sh.kchunk);
+    }
+    float* sum = out;
+    if (!sum) {
+        rc = hip_rc(fc::noalloc_scratch(dev, &sum));
+        if (rc) return rc;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    bool note = false;
+    rc = order_after_last(p, s, note);
+    if (rc) return rc;
+    rc = update_step_tables(p, grads, bcast_dst, s);
+    if (rc == FC_OK)
+        rc = two_pass(p, sh, sum, w, v, lr, mu, wd, 1.0f / static_cast<float>(batch), bcast_dst != nullptr, s,
+                      false);
+    if (note) note_stream(p, s);
+    return rc;
+}
+
 uint64_t fc_read_probe_blocks(uint64_t bytes) { return fc::read_probe_blocks(bytes); }
 
 int fc_read_probe(const void* src, uint64_t bytes, float* out, void* stream) {
@@ -968,6 +1007,12 @@ int fc_broadcast(fc_plan* p, const float* src, float* const* dst, void* stream) 
 int fc_step(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd, int batch,
             float* out, float* const* bcast_dst, void* stream) {
     return guarded([&] { return fc_step_body(p, grads, w, v, lr, mu, wd, batch, out, bcast_dst, stream); });
+}
+
+int fc_step_noalloc(fc_plan* p, const void* const* grads, float* w, float* v, float lr, float mu, float wd,
+                    int batch, float* out, float* const* bcast_dst, void* stream) {
+    // no try/catch here: nothing on this path allocates or throws
+    return fc_step_noalloc_body(p, grads, w, v, lr, mu, wd, batch, out, bcast_dst, stream);
 }
 
 int fc_plan_balance(fc_plan* p, void* stream, float* xcd_rate, int n_rate) {

@@ -104,6 +104,10 @@ hipError_t prepare_resident_f16(const Shape& sh, size_t lds);
 hipError_t launch_resident_f32(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a, hipStream_t s);
 hipError_t launch_resident_f16(const Shape& sh, int mode, int grid, size_t lds, const ResidentArgs& a, hipStream_t s);
 uint64_t read_probe_blocks(uint64_t bytes);
+
+// Device address, on `device` (which must be the current device), of the
+// fixed raw-sum array of fc_step_noalloc (FC_NOALLOC_MAX_ELEMS floats).
+hipError_t noalloc_scratch(int device, float** ptr);
 hipError_t launch_read_probe(const void* src, uint64_t bytes, float* out, hipStream_t s);
 
 }  // namespace fc

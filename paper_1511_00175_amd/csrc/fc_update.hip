@@ -1,10 +1,36 @@
 // SGD-from-a-raw-sum and broadcast kernels: one block per tile, one thread
 // per lane of the tile; on resident plans the broadcast runs one persistent
 // block per CU.
+#include <mutex>
+
 #include "fc_device.h"
 
 namespace fc {
 
+// The raw sum between the two passes of fc_step_noalloc: a fixed array that
+// the HIP runtime places on every GPU the library's code is loaded on and
+// keeps until the process ends, so that the call itself allocates nothing.
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) float scratch[FC_NOALLOC_MAX_ELEMS];
+
+constexpr int NOALLOC_MAX_DEVICES = 64;
+
+hipError_t noalloc_scratch(int device, float** ptr) {
+    static std::mutex mu;
+    static float* address[NOALLOC_MAX_DEVICES] = {};
+    if (device < 0 || device >= NOALLOC_MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> hold(mu);
+    if (!address[device]) {
+        void* a = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!a) return hipErrorInvalidSymbol;
+        address[device] = static_cast<float*>(a);
+    }
+    *ptr = address[device];
+    return hipSuccess;
+}
 
 hipError_t launch_sgd(const Shape& sh, int grid, const SgdArgs& a, hipStream_t s) {
     auto go = [&](auto u) {

@@ -38,6 +38,7 @@ def test_valid_buffers_reach_the_library(fc):
     r, w, v, out, dst = bufs()
     reaches_library(fc, lambda: p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0))
     reaches_library(fc, lambda: p.step(list(r), w, v, 0.1, 0.9, 0.0, 1, out=out, bcast=dst, stream=0))
+    reaches_library(fc, lambda: p.step_noalloc(r, w, v, 0.1, 0.9, 0.0, 1, bcast=list(dst), stream=0))
     reaches_library(fc, lambda: p.tree_reduce(r[:, :1000], out, stream=0))
     reaches_library(fc, lambda: p.sgd_step(w, v, out, 0.1, 0.9, 0.0, 1, stream=0))
     reaches_library(fc, lambda: p.broadcast(out, dst, stream=0))
@@ -96,3 +97,5 @@ def test_other_calls_check_their_buffers(fc):
         p.broadcast(out, dst[:, :10])
     with pytest.raises(ValueError):
         p.train(r.half(), w, v, dict(kind="fixed", base_lr=0.1), 0, 1, 0.9, 0.0, 1)
+    with pytest.raises(ValueError):
+        p.step_noalloc(r, w, v[:3], 0.1, 0.9, 0.0, 1)
