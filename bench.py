@@ -12,10 +12,13 @@ earlier steps' w and v in the Infinity Cache.
 
 Prints ONE JSON line: effective HBM GB/s of the step (algorithmic bytes per
 step / wall time per step over the timed steps), the roofline entry of the
-dominant kernel (its algorithmic bytes per step / its time per step from HIP
+dominant kernel (its algorithmic bytes per call / its call time from HIP
 events the library records on the launch stream around each call, all of the
-call's launches included, against the 8 TB/s HBM3E peak), and the oracle
-timed on the host cores as a CPU baseline.
+call's launches included, against the 8 TB/s HBM3E peak; beside it the
+kernel time rocprofv3 recorded for the same sources, when committed), a
+parity verdict (one more step of the timed plan, outside the timed regions,
+compared bit for bit with the oracle on every element) and the oracle timed
+on the host cores as a CPU baseline.  Exits with status 1 when parity fails.
 
     python bench.py [--workload googlenet] [--steps 200] [--warmup 20]
 """
@@ -111,6 +114,77 @@ def read_traffic(workload, kernel):
         return None
 
 
+def read_profile_us(workload, kernel):
+    """Average kernel time per step (us) that rocprofv3 recorded for `kernel`
+    in profiles/traffic_<workload>.txt, or None when absent or taken on
+    another version of the kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("kernel") != kernel:
+        return None
+    try:
+        return float(kv["rocprof_us_per_step"])
+    except (KeyError, ValueError):
+        return None
+
+
+def mismatches(a, b):
+    """Elements whose bits differ (any NaN equal to any NaN)."""
+    import numpy as np
+    a, b = np.asarray(a, dtype=np.float32).ravel(), np.asarray(b, dtype=np.float32).ravel()
+    nan = np.isnan(a) & np.isnan(b)
+    return int(np.count_nonzero(~nan & (a.view(np.uint32) != b.view(np.uint32))))
+
+
+def parity_check(plan, wl, reps, wv, order, out, bcast):
+    """One more step of the timed plan (shares as timed) on replica set 0 and
+    on copies of (w, v) set 0 as the timed steps left it, outside the timed regions,
+    against the oracle run on host copies of the same inputs (every host
+    thread, one range of elements each): every element of w', v' (and of
+    the raw sum and the K worker copies when the step writes them), padding
+    included.  Returns the JSON object and the host copies of the inputs."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    w, v = wv[0].clone(), wv[1].clone()
+    reps_h, w_h, v_h = reps.cpu().numpy(), w.cpu().numpy(), v.cpu().numpy()
+    n = w.numel()
+    out_d = torch.full((n,), -1.0, device=w.device) if out else None
+    dst_d = torch.full((wl.K, n), -2.0, device=w.device) if bcast else None
+    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out_d, bcast=dst_d)
+    torch.cuda.synchronize()
+    out_h = np.full(n, -1.0, np.float32) if out else None
+    dst_h = [np.full(n, -2.0, np.float32) for _ in range(wl.K)] if bcast else None
+    threads = oracle.default_threads()
+    t0 = time.perf_counter()
+    ew, ev, _, _ = oracle.step_parallel(wl.table(), reps_h, w_h, v_h, wl.lr, wl.mu, wl.wd, wl.batch, order=order,
+                                        out=out_h, bcast=dst_h, threads=threads)
+    dt = time.perf_counter() - t0
+    bad = mismatches(w.cpu().numpy(), ew) + mismatches(v.cpu().numpy(), ev)
+    names = ["w", "v"]
+    if out:
+        bad += mismatches(out_d.cpu().numpy(), out_h)
+        names.append("raw sum")
+    if bcast:
+        bad += sum(mismatches(dst_d[k].cpu().numpy(), dst_h[k]) for k in range(wl.K))
+        names.append(f"{wl.K} worker copies")
+    elements = n * (2 + (1 if out else 0) + (wl.K if bcast else 0))
+    res = {"bit_exact": bad == 0, "elements": elements, "mismatches": bad, "outputs": names,
+           "checked": f"every element of {', '.join(names)} ({n} per buffer, padding included) after one "
+                      "more step of the timed plan, against the oracle on the same inputs",
+           "oracle": f"oracle.step_parallel, {threads} host threads", "oracle_seconds": round(dt, 3)}
+    return res, (reps_h, w_h, v_h)
+
+
 def host_info():
     model = platform.processor() or ""
     try:
@@ -124,66 +198,28 @@ def host_info():
     return model, os.cpu_count()
 
 
-def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
-    """Time the oracle (one host core) on a contiguous window of the
-    workload's elements, all K replicas; returns the JSON object."""
-    import numpy as np
-    import torch
-
+def cpu_baseline(wl, reps_h, w_h, v_h, order, target_s=10.0):
+    """Time the oracle on a contiguous window [0, m) of the workload's
+    elements, all K replicas, from host copies of the inputs: once on one
+    host core (oracle.step; the window grown to about target_s seconds, or
+    the whole step), then on every host thread (oracle.step_parallel: one
+    range of elements per thread, the same arithmetic for every element),
+    best of 3.  Returns the JSON object."""
     import oracle
 
-    segs = oracle.segments(wl.table())
-    ends = segs["offset"] + segs["length"]
+    table = wl.table()
 
     def window(m):
         # segments clipped to [0, m)
-        rows = []
-        for (o, n, lm, dm), e in zip(wl.table(), ends):
-            if o >= m:
-                break
-            rows.append((o, min(n, m - o), lm, dm))
-        return rows
+        return [(o, min(n, m - o), lm, dm) for o, n, lm, dm in table if o < m]
 
     def run(m):
         rows = window(m)
-        r = reps[:, :m].cpu().numpy()
-        wh = w[:m].cpu().numpy()
-        vh = v[:m].cpu().numpy()
         t0 = time.perf_counter()
-        oracle.step(rows, list(r), wh, vh, wl.lr, wl.mu, wl.wd, wl.batch, order=order)
-        dt = time.perf_counter() - t0
-        return dt, sum(n for _, n, _, _ in rows)
+        oracle.step(rows, list(reps_h[:, :m]), w_h[:m], v_h[:m], wl.lr, wl.mu, wl.wd, wl.batch, order=order)
+        return time.perf_counter() - t0, sum(n for _, n, _, _ in rows)
 
-    def run_threads(m, nthreads, repeats=3):
-        # the same window cut into element ranges, one oracle call per range
-        # on its own host thread (ctypes releases the GIL); every element's
-        # arithmetic and order are unchanged
-        from concurrent.futures import ThreadPoolExecutor
-        rows = window(m)
-        r = reps[:, :m].cpu().numpy()
-        wh = w[:m].cpu().numpy()
-        vh = v[:m].cpu().numpy()
-        cuts = [m * i // nthreads for i in range(nthreads + 1)]
-        jobs = []
-        for a, b in zip(cuts[:-1], cuts[1:]):
-            sub = [(max(o, a) - a, min(o + n, b) - max(o, a), lm, dm) for (o, n, lm, dm) in rows
-                   if max(o, a) < min(o + n, b)]
-            if sub:
-                jobs.append((sub, [r[k, a:b] for k in range(r.shape[0])], wh[a:b], vh[a:b]))
-
-        def one(job):
-            sub, rr, ww, vv = job
-            oracle.step(sub, rr, ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, order=order)
-
-        best = float("inf")
-        with ThreadPoolExecutor(nthreads) as ex:
-            for _ in range(repeats):
-                t0 = time.perf_counter()
-                list(ex.map(one, jobs))
-                best = min(best, time.perf_counter() - t0)
-        return best
-
-    total = int(ends.max())
+    total = max(o + n for o, n, _, _ in table)
     m = min(total, 1 << 16)
     dt, n = run(m)
     # grow the window to about target_s seconds of single-thread oracle work
@@ -193,9 +229,14 @@ def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
         m = m2
     bytes_ = n * (wl.K * wl.s_g + 16)
     model, ncpu = host_info()
-    # the host's CPU share: OMP_NUM_THREADS when set, else every core
-    nthreads = max(1, min(ncpu or 1, int(os.environ.get("OMP_NUM_THREADS", ncpu or 1))))
-    dt_mt = run_threads(m, nthreads)
+    nthreads = oracle.default_threads()
+    rows = window(m)
+    dt_mt = float("inf")
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.step_parallel(rows, reps_h[:, :m], w_h[:m], v_h[:m], wl.lr, wl.mu, wl.wd, wl.batch, order=order,
+                             threads=nthreads)
+        dt_mt = min(dt_mt, time.perf_counter() - t0)
     return {"value": round(bytes_ / dt_mt / 1e9, 4), "unit": "GB/s", "cores": nthreads, "kind": "oracle",
             "sample": f"{n} of {wl.n_params} parameters (elements [0, {m}) of the layout), all K={wl.K} "
                       f"replicas, one fused step, cut into {nthreads} element ranges run on {nthreads} host "
@@ -204,34 +245,35 @@ def cpu_baseline(wl, reps, w, v, order, target_s=10.0):
             "single_thread": {"value": round(bytes_ / dt / 1e9, 4), "seconds": round(dt, 3), "cores": 1}}
 
 
-def sweep_k(args):
+FIG4_KS = (1, 2, 4, 8, 16, 32, 64, 128)
+
+
+def sweep_k(n, ks=FIG4_KS, reps_per_k=20, seed=1511, samples=1 << 16):
     """One-GPU analog of Fig. 4 (parameter server vs reduction tree, NiN's 30 MB
-    per worker): for K = 1..128 workers, time fc_tree_reduce in tree and in
-    linear (parameter-server) order over one 7,595,176-parameter (NiN-sized)
-    fp32 vector per worker, and measure each order's rounding error against an
-    fp64 sum.  On one GPU both orders read the same K*N*4 bytes, so time grows
-    linearly in K for both (Eq. 3 vs Eq. 4 is a network cost model); what the
-    order changes is the error bound: gamma_d * sum|x| with d = ceil(log2 K)
-    for the tree, d = K-1 for the linear order.  Prints one JSON line per
-    (K, order)."""
+    per worker at n = 7,595,176): for each K, time fc_tree_reduce in tree and
+    in linear (parameter-server) order over one n-element fp32 vector per
+    worker, and measure each order's rounding error against an fp64 sum on
+    `samples` sampled elements.  On one GPU both orders read the same K*n*4
+    bytes, so time grows linearly in K for both (Eq. 3 vs Eq. 4 is a network
+    cost model); what the order changes is the error bound: |s - exact| <=
+    gamma_d * sum|x| with d = ceil(log2 K) for the tree, d = K-1 for the
+    linear order.  Returns one record per (K, order)."""
     import torch
 
     import paper_1511_00175_amd as fc
-    from workloads import tables
 
     dev = torch.device("cuda:0")
-    wl = tables.nin()
-    n = wl.n_params
     g = torch.Generator(device=dev)
-    g.manual_seed(args.seed)
-    kmax = 128
+    g.manual_seed(seed)
+    kmax = max(ks)
     stride = (n + 63) // 64 * 64 + 64  # 256-byte aligned replica rows, staggered
     reps = (torch.randn((kmax, stride), generator=g, device=dev) * 1e-3)
     out = torch.empty(n, device=dev)
     rows = [(0, n, 1.0, 1.0)]
-    sample = torch.randint(0, n, (1 << 16,), generator=g, device=dev)
+    sample = torch.randint(0, n, (min(samples, n),), generator=g, device=dev)
     u = 2.0 ** -24
-    for K in (1, 2, 4, 8, 16, 32, 64, 128):
+    recs = []
+    for K in ks:
         x = reps[:K]
         exact = x[:, sample].double().sum(0)
         absum = x[:, sample].double().abs().sum(0)
@@ -241,7 +283,7 @@ def sweep_k(args):
             for _ in range(3):
                 plan.tree_reduce(x, out)
             plan.read_timing()
-            for _ in range(args.sweep_reps):
+            for _ in range(reps_per_k):
                 plan.tree_reduce(x, out)
             torch.cuda.synchronize()
             launches, total = plan.read_timing()["reduce"]
@@ -249,11 +291,12 @@ def sweep_k(args):
             rel = ((out[sample].double() - exact).abs() / absum).cpu()
             d = 0 if K == 1 else (math.ceil(math.log2(K)) if order == "tree" else K - 1)
             us = total / launches
-            print(json.dumps({"sweep": "fig4_one_gpu", "K": K, "order": order, "n_params": n,
-                              "mb_per_worker": round(4 * n / 1e6, 1), "us": round(us, 2),
-                              "gb_s": round((K * 4 + 4) * n / us / 1e3, 1),
-                              "err_rel_median": float(rel.median()), "err_rel_max": float(rel.max()),
-                              "bound_gamma_d": d * u / (1 - d * u)}), flush=True)
+            recs.append({"sweep": "fig4_one_gpu", "K": K, "order": order, "n_params": n,
+                         "mb_per_worker": round(4 * n / 1e6, 1), "us": round(us, 2),
+                         "gb_s": round((K * 4 + 4) * n / us / 1e3, 1),
+                         "err_rel_median": float(rel.median()), "err_rel_max": float(rel.max()),
+                         "bound_gamma_d": d * u / (1 - d * u)})
+    return recs
 
 
 def input_hash(sets, wv):
@@ -343,11 +386,14 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="googlenet",
-                    choices=["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux", "alexnet_ungrouped"])
+                    choices=["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux", "googlenet_caffe_bias",
+                             "alexnet_ungrouped"])
     ap.add_argument("--order", default="tree", choices=["tree", "linear"])
     ap.add_argument("--out", action="store_true", help="also write the raw sum")
     ap.add_argument("--bcast", action="store_true", help="also broadcast w' to K worker copies")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true",
+                    help="skip the parity check (one more step against the oracle on every element)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--seed", type=int, default=1511)
     ap.add_argument("--opts", default="", help="launch shape, e.g. block_threads=256,vecs_per_thread=1")
@@ -394,7 +440,10 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(2)
     if args.sweep_k:
-        sweep_k(args)
+        from workloads import tables as _t
+        for rec in sweep_k(_t.nin().n_params, reps_per_k=args.sweep_reps, seed=args.seed):
+            rec["kernel_source_sha256_16"] = kernel_hash()
+            print(json.dumps(rec), flush=True)
         return
     dev = torch.device("cuda:0")
     wl = tables.get(args.workload)
@@ -498,18 +547,22 @@ def main():
     bytes_step = wl.algorithmic_bytes(out=args.out, bcast=args.bcast)
     ms_per_step = wall / args.steps * 1e3
     value = bytes_step / (wall / args.steps) / 1e9
-    kernels = {k: {"launches": n, "avg_us": round(us / n, 2),
+    # per kernel kind: calls, and the mean time between the HIP events the
+    # library records around each call on its launch stream (all of a call's
+    # launches: one per resident round)
+    kernels = {k: {"calls": n, "call_us_avg": round(us / n, 2),
                    "algorithmic_bytes": kernel_bytes(wl, k, args.out, bcast=args.bcast and k != "reduce")}
                for k, (n, us) in timing.items() if n}
     if not kernels:  # no per-kernel events: the whole step stands in for its kernels
-        kernels = {"step": {"launches": args.steps, "avg_us": round(ms_per_step * 1e3, 2),
+        kernels = {"step": {"calls": args.steps, "call_us_avg": round(ms_per_step * 1e3, 2),
                             "algorithmic_bytes": bytes_step}}
-    dom = max(kernels, key=lambda k: kernels[k]["launches"] * kernels[k]["avg_us"])
-    avg = kernels[dom]["avg_us"] * 1e-6
+    dom = max(kernels, key=lambda k: kernels[k]["calls"] * kernels[k]["call_us_avg"])
+    avg = kernels[dom]["call_us_avg"] * 1e-6
     achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
     plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE or
                  args.no_balance or args.wv_sets)
     traffic = read_traffic(wl.name, dom) if plain else None
+    prof_us = read_profile_us(wl.name, dom) if plain else None
     sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
     rk = "resident_kernel" if info.schedule == 3 else "reduce_kernel"
 
@@ -554,7 +607,13 @@ def main():
             "traffic": traffic,
             "kernel": {"step": f"fc::{rk} (fused step)", "reduce": f"fc::{rk} (reduce pass)",
                        "sgd": "fc::sgd_kernel", "bcast": "fc::bcast_kernel"}[dom],
-            "kernel_us_avg": round(avg * 1e6, 2),
+            "call_us_avg": round(avg * 1e6, 2),
+            "timing": "HIP events recorded by the library on the launch stream around each call of the "
+                      "dominant kernel kind over timed region 2",
+            "launches_per_call": info.rounds if info.schedule == 3 and dom in ("step", "reduce") else 1,
+            "kernel_us_avg": prof_us,
+            "kernel_us_source": "rocprofv3 kernel trace committed in profiles/ for these kernel sources"
+                                if prof_us else None,
             "kernel_algorithmic_bytes": kernels[dom]["algorithmic_bytes"],
         },
         "cpu_baseline": None,
@@ -572,11 +631,20 @@ def main():
                                           "frac": round(model_us / (ms_per_step * 1e3), 4)}
     if graph:
         res["graph"] = graph
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl, reps, w, v, args.order, args.cpu_seconds)
+    res["parity"] = None
+    host_copies = None
+    if not args.no_parity:
+        res["parity"], host_copies = parity_check(plans[0], wl, sets[0][0], wv[0], args.order, args.out, args.bcast)
     for p in plans:
         p.close()
+    if not args.no_cpu_baseline:
+        if host_copies is None:
+            host_copies = (sets[0][0].cpu().numpy(), wv[0][0].cpu().numpy(), wv[0][1].cpu().numpy())
+        res["cpu_baseline"] = cpu_baseline(wl, *host_copies, args.order, args.cpu_seconds)
     print(json.dumps(res), flush=True)
+    if res["parity"] is not None and not res["parity"]["bit_exact"]:
+        print(f"bench.py: {res['parity']['mismatches']} elements differ from the oracle", file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -183,6 +183,64 @@ def step(segs, grads, w, v, lr, mu, wd, batch, order="tree", out=None, bcast=Non
     return w, v, out, bcast
 
 
+def default_threads():
+    """Host threads for step_parallel: OMP_NUM_THREADS when set (the GPU machine
+    sets it to its CPU share), else every core."""
+    n = os.cpu_count() or 1
+    return max(1, min(n, int(os.environ.get("OMP_NUM_THREADS", n))))
+
+
+def step_parallel(segs, grads, w, v, lr, mu, wd, batch, order="tree", out=None, bcast=None, threads=None):
+    """The fused step of `step`, run by `threads` host threads, each calling
+    the same C function on one contiguous range of element indices.
+
+    Every parameter's sum and update read and write only that parameter's
+    element of each buffer (the workers' vectors are added element by element,
+    Sec. 6.2), so cutting the index range changes no element's operations or
+    their order: the result is the one `step` computes.  `grads` is a 2-D
+    array (K, n) or a list of K 1-D arrays.  Returns (w', v', out, bcast) like
+    `step`; `out` and the arrays of `bcast` are updated in place."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    t = segments(segs)
+    reps, dt = _replicas(list(grads))
+    K = len(reps)
+    w = np.array(w, dtype=np.float32, copy=True)
+    v = np.array(v, dtype=np.float32, copy=True)
+    if bcast is not None:
+        for d in bcast:
+            assert d.dtype == np.float32 and d.flags.c_contiguous
+    n = extent(t)
+    threads = threads or default_threads()
+    cuts = sorted(set(n * i // threads for i in range(threads + 1)))
+    L = lib()
+
+    def addr(a, first):
+        return a.ctypes.data + first * a.itemsize
+
+    def run(a, b):
+        # the segments clipped to [a, b), offsets relative to a
+        rows = [(max(o, a) - a, min(o + m, b) - max(o, a), lm, dm)
+                for o, m, lm, dm in zip(t["offset"].tolist(), t["length"].tolist(), t["lr_mult"].tolist(),
+                                        t["decay_mult"].tolist())
+                if max(o, a) < min(o + m, b)]
+        if not rows:
+            return 0
+        sub = segments(rows)
+        scratch = np.empty(b - a, dtype=np.float32)
+        rt = (ctypes.c_void_p * K)(*[addr(r, a) for r in reps])
+        bt = (ctypes.c_void_p * K)(*[addr(d, a) for d in bcast]) if bcast is not None else None
+        return L.orc_step(_ptr(sub), len(sub), K, dt, ORDERS[order], rt, ctypes.c_void_p(addr(w, a)),
+                          ctypes.c_void_p(addr(v, a)), lr, mu, wd, int(batch), _ptr(scratch),
+                          ctypes.c_void_p(addr(out, a)) if out is not None else None, bt)
+
+    with ThreadPoolExecutor(max(1, len(cuts) - 1)) as ex:
+        codes = list(ex.map(lambda ab: run(*ab), zip(cuts[:-1], cuts[1:])))
+    if any(codes):
+        raise ValueError(f"orc_step failed ({codes})")
+    return w, v, out, bcast
+
+
 LR_KINDS = {"fixed": 0, "step": 1, "poly": 2}
 
 

@@ -62,3 +62,41 @@ def test_traffic_profiles_name_their_kernel_and_bytes():
         assert len(kv["kernel_source_sha256_16"]) == 16
         ratio = float(kv["hbm_bytes_per_step"]) / float(kv["algorithmic_bytes_per_step"])
         assert 0.99 < ratio < 1.03, (name, ratio)
+
+
+def test_mismatches_compares_bits():
+    import numpy as np
+
+    import bench
+    a = np.array([0.0, -0.0, 1.0, np.nan, 2.0], np.float32)
+    b = np.array([0.0, 0.0, 1.0, np.nan, np.nextafter(np.float32(2.0), np.float32(3.0))], np.float32)
+    assert bench.mismatches(a, a) == 0
+    assert bench.mismatches(a, b) == 2  # -0 vs +0, and one ulp
+
+
+def test_cpu_baseline_times_the_oracle_on_host_copies():
+    """The baseline leg runs the oracle on one core and on every host thread
+    over the same window of host copies and reports the thread count."""
+    import bench
+    from workloads import gen, tables
+    wl = tables.flat()
+    reps, w, v = gen.host_inputs(wl, 3)
+    r = bench.cpu_baseline(wl, reps, w, v, "tree", target_s=0.05)
+    assert r["kind"] == "oracle" and r["unit"] == "GB/s" and r["value"] > 0 and r["cores"] >= 1
+    assert r["single_thread"]["cores"] == 1 and f"{r['cores']} host threads" in r["sample"]
+
+
+def test_profile_time_needs_the_current_sources(tmp_path, monkeypatch):
+    """roofline.kernel_us_avg comes from a committed profile only when it was
+    taken on the current kernel sources."""
+    import bench
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    (prof / "traffic_x.txt").write_text(f"kernel: step\nkernel_source_sha256_16: {bench.kernel_hash()}\n"
+                                        "rocprof_us_per_step: 12.5\n")
+    assert bench.read_profile_us("x", "step") == 12.5
+    assert bench.read_profile_us("x", "reduce") is None
+    (prof / "traffic_x.txt").write_text("kernel: step\nkernel_source_sha256_16: 0000000000000000\n"
+                                        "rocprof_us_per_step: 12.5\n")
+    assert bench.read_profile_us("x", "step") is None

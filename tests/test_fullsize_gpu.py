@@ -1,18 +1,19 @@
-"""Parity at the full workload sizes, in the launch configuration bench.py
-times (the plan defaults, resident shares rebalanced per XCD after the first
-step as bench.py does after its warm-up), on sampled outputs the oracle
-computes one by one.
+"""Parity at the full workload sizes on every element, in the launch
+configuration bench.py times (the plan defaults, resident shares rebalanced
+per XCD after the first step as bench.py does after its warm-up).
 
-For each of the five workloads (flat 2^20 x K=4, NiN x K=32, GoogLeNet
-x K=128, VGG-19 x K=16, AlexNet fp16 x K=128), and Table 1's variants
-(GoogLeNet with its auxiliary classifiers, ungrouped AlexNet), the inputs are drawn on the
-device, three fused steps run on the GPU (fc_plan_balance after the first),
-and at every segment's first, second, last and one random element plus 1500
-random elements the oracle recomputes the same three steps from the gathered
-inputs; w' and v' must match bit for bit.
-Properties that hold at any size are checked on the whole buffer: the fused
-step equals reduce, then SGD (GoogLeNet), and the broadcast copies and raw
-sum fused into the step equal w' and the reduce's sum (GoogLeNet, VGG-19).
+For each workload -- flat 2^20 x K=4, NiN x K=32, GoogLeNet x K=128, VGG-19
+x K=16, AlexNet fp16 x K=128 in tree and in parameter-server order, and Table
+1's variants (GoogLeNet with its auxiliary classifiers, GoogLeNet with
+Caffe's bias multipliers, ungrouped AlexNet) -- the inputs are drawn on the
+device and copied to the host, three steps run on the GPU (fc_plan_balance
+after the first), and the oracle runs the same three steps on the host copies
+on every host thread (oracle.step_parallel: one range of elements per thread,
+the same scalar arithmetic for every element).  Every element of w' and v',
+the padding between segments included (which neither side may write), must
+match bit for bit.  GoogLeNet (K = 128 copies, one resident round) and
+VGG-19 (K = 16 copies, 14 rounds) also run steps that keep the raw sum and
+broadcast w' into the K worker copies: every element of those too.
 """
 import numpy as np
 import pytest
@@ -30,54 +31,68 @@ def fc(device):
     return m
 
 
-def sample_indices(wl, rng, n_random=1500):
-    """Each segment's first, second, last and one random element, plus
-    n_random elements drawn with probability proportional to segment length."""
-    idx = []
-    for s in wl.segments:
-        idx += [s.offset, s.offset + min(1, s.length - 1), s.offset + s.length - 1,
-                s.offset + int(rng.integers(0, s.length))]
-    lens = np.array([s.length for s in wl.segments], dtype=np.float64)
-    js = rng.choice(len(wl.segments), n_random, p=lens / lens.sum())
-    idx += [wl.segments[j].offset + int(rng.integers(0, wl.segments[j].length)) for j in js]
-    return np.unique(np.array(idx, dtype=np.int64))
+def host(t):
+    return t.cpu().numpy()
 
 
-def segment_of(wl, idx):
-    offs = np.array([s.offset for s in wl.segments])
-    return np.searchsorted(offs, idx, side="right") - 1
-
-
-@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux",
-                                  "alexnet_ungrouped"])
-def test_fullsize_sampled(fc, name):
+@pytest.mark.parametrize("name,order", [
+    ("flat", "tree"), ("nin", "tree"), ("googlenet", "tree"), ("vgg19", "tree"), ("alexnet", "tree"),
+    ("alexnet", "linear"), ("googlenet_aux", "tree"), ("googlenet_caffe_bias", "tree"),
+    ("alexnet_ungrouped", "tree")])
+def test_fullsize_every_element(fc, name, order):
     import torch
     wl = tables.get(name)
     dev = torch.device("cuda:0")
-    rng = np.random.default_rng(len(name))
     reps, w, v = gen.device_inputs(wl, 1511, dev)
-    idx = sample_indices(wl, rng)
-    it = torch.from_numpy(idx).to(dev)
-    g_s = reps[:, it].cpu().numpy()                 # (K, S) gathered replica values
-    w_s, v_s = w[it].cpu().numpy(), v[it].cpu().numpy()
-    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
+    reps_h, w_h, v_h = host(reps), host(w), host(v)
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, order)
     for i in range(3):
         plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
         if i == 0:
             plan.balance()
     torch.cuda.synchronize()
-    got_w, got_v = w[it].cpu().numpy(), v[it].cpu().numpy()
     plan.close()
+    got_w, got_v = host(w), host(v)
     del reps, w, v
     torch.cuda.empty_cache()
-    # oracle on the gathered samples: each sample is a one-element segment
-    # carrying its own segment's multipliers
-    js = segment_of(wl, idx)
-    rows = [(i, 1, wl.segments[j].lr_mult, wl.segments[j].decay_mult) for i, j in enumerate(js)]
-    ew, ev = w_s, v_s
+    ew, ev = w_h, v_h
     for _ in range(3):
-        ew, ev, _, _ = oracle.step(rows, list(g_s), ew, ev, wl.lr, wl.mu, wl.wd, wl.batch)
+        ew, ev, _, _ = oracle.step_parallel(wl.table(), reps_h, ew, ev, wl.lr, wl.mu, wl.wd, wl.batch, order=order)
     assert same_bits(got_w, ew) == 0 and same_bits(got_v, ev) == 0
+
+
+@pytest.mark.parametrize("name", ["googlenet", "vgg19"])
+def test_fullsize_sum_and_broadcast(fc, name):
+    """Two steps that also keep the raw sum and broadcast w' to the K worker
+    copies, shares rebalanced per XCD between them: w', v', the raw sum and
+    every copy against the oracle on every element (outside the segments the
+    copies and the sum keep their fill values)."""
+    import torch
+    wl = tables.get(name)
+    dev = torch.device("cuda:0")
+    reps, w, v = gen.device_inputs(wl, 5, dev)
+    reps_h, w_h, v_h = host(reps), host(w), host(v)
+    n = w.numel()
+    dst = torch.full((wl.K, n), -2.0, device=dev)
+    out = torch.full((n,), -1.0, device=dev)
+    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
+    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=dst)
+    plan.balance()
+    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=dst)
+    torch.cuda.synchronize()
+    plan.close()
+    out_h = np.full(n, -1.0, np.float32)
+    dst_h = [np.full(n, -2.0, np.float32) for _ in range(wl.K)]
+    ew, ev = w_h, v_h
+    for _ in range(2):
+        ew, ev, _, _ = oracle.step_parallel(wl.table(), reps_h, ew, ev, wl.lr, wl.mu, wl.wd, wl.batch,
+                                            out=out_h, bcast=dst_h)
+    assert same_bits(host(w), ew) == 0 and same_bits(host(v), ev) == 0
+    assert same_bits(host(out), out_h) == 0
+    for k in range(wl.K):
+        assert same_bits(host(dst[k]), dst_h[k]) == 0, k
+    del reps, w, v, dst, out
+    torch.cuda.empty_cache()
 
 
 def test_fullsize_fused_equals_composed(fc):
@@ -100,44 +115,6 @@ def test_fullsize_fused_equals_composed(fc):
     assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
     assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
     plan.close()
-
-
-@pytest.mark.parametrize("name", ["googlenet", "vgg19"])
-def test_fullsize_broadcast(fc, name):
-    """The raw sum and the broadcast of w' fused into the step at full size
-    (GoogLeNet: K = 128 copies, one resident round; VGG-19: K = 16 copies,
-    14 rounds), shares rebalanced per XCD after it: every worker copy equals
-    w' bit for bit on every parameter and keeps its fill value on the
-    padding, the raw sum equals fc_tree_reduce's, and w', v' equal those of
-    a step without either (properties that hold at any size)."""
-    import torch
-    wl = tables.get(name)
-    dev = torch.device("cuda:0")
-    reps, w, v = gen.device_inputs(wl, 5, dev)
-    w2, v2 = w.clone(), v.clone()
-    n = w.numel()
-    mask = torch.zeros(n, dtype=torch.bool, device=dev)
-    for s in wl.segments:
-        mask[s.offset:s.offset + s.length] = True
-    dst = torch.full((wl.K, n), -2.0, device=dev)
-    out = torch.full((n,), -1.0, device=dev)
-    g = torch.full((n,), -1.0, device=dev)
-    plan = fc.Plan(wl.table(), wl.K, wl.dtype, "tree")
-    plan.step(reps, w, v, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=dst)
-    plan.balance()
-    plan.step(reps, w2, v2, wl.lr, wl.mu, wl.wd, wl.batch)
-    plan.tree_reduce(reps, g)
-    torch.cuda.synchronize()
-    plan.close()
-    assert torch.equal(w.view(torch.int32), w2.view(torch.int32))
-    assert torch.equal(v.view(torch.int32), v2.view(torch.int32))
-    assert torch.equal(out.view(torch.int32), g.view(torch.int32))
-    wm = w[mask].view(torch.int32)
-    for k in range(wl.K):
-        assert torch.equal(dst[k][mask].view(torch.int32), wm), k
-        assert bool((dst[k][~mask] == -2.0).all()), k
-    del reps, w, v, w2, v2, dst, out, g
-    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("dtype,schedule", [("f16", 1), ("f16", 3), ("f32", 2), ("f32", 3)])

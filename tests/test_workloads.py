@@ -27,8 +27,8 @@ def test_shapes(name, nseg, nparams, minseg):
     assert min(s.length for s in wl.segments) == minseg
 
 
-@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "googlenet_aux", "vgg19", "alexnet",
-                                  "alexnet_ungrouped"])
+@pytest.mark.parametrize("name", ["flat", "nin", "googlenet", "googlenet_aux", "googlenet_caffe_bias", "vgg19",
+                                  "alexnet", "alexnet_ungrouped"])
 def test_layout_rules(name):
     wl = tables.get(name)
     end = 0
@@ -65,3 +65,14 @@ def test_algorithmic_bytes():
     assert wl.algorithmic_bytes() == wl.n_params * (128 * 4 + 16)
     assert wl.algorithmic_bytes(out=True, bcast=True) == wl.n_params * (128 * 4 + 16 + 4 + 4 * 128)
     assert tables.alexnet().algorithmic_bytes() == 60_965_224 * (128 * 2 + 16)
+
+
+def test_caffe_bias_variant():
+    """GoogLeNet with Caffe's bias multipliers: the layout of GoogLeNet, every
+    bias segment (2, 0), every weight segment (1, 1)."""
+    a, b = tables.googlenet(), tables.get("googlenet_caffe_bias")
+    assert [(s.offset, s.length) for s in a.segments] == [(s.offset, s.length) for s in b.segments]
+    assert b.name == "googlenet_caffe_bias" and b.n_params == a.n_params
+    for s in b.segments:
+        assert (s.lr_mult, s.decay_mult) == ((2.0, 0.0) if s.is_bias else (1.0, 1.0))
+    assert sum(1 for s in b.segments if s.is_bias) == 58

@@ -157,9 +157,9 @@ def alexnet_layers(grouped=True):
             conv("fc6", 4096, 9216), conv("fc7", 4096, 4096), conv("fc8", 1000, 4096)]
 
 
-def _make(name, layers, **kw):
+def _make(name, layers, caffe_bias_mults=False, **kw):
     wl = Workload(name=name, layers=layers, **kw)
-    wl.segments, wl.padded = lay_out(layers)
+    wl.segments, wl.padded = lay_out(layers, caffe_bias_mults=caffe_bias_mults)
     return wl
 
 
@@ -179,10 +179,14 @@ def nin():
                  grad_std="fan_in", weight_init="nin")
 
 
-def googlenet(aux=False):
+def googlenet(aux=False, caffe_bias=False):
     """GoogLeNet v1 shapes (57 convolutions + FC), K=128 fp32, batch 1024,
-    lr 0.08 (Sec. 7.3 "Ultra-deep models"), mu 0.9, wd 2e-4 (Sec. 7.1)."""
-    return _make("googlenet" + ("_aux" if aux else ""), googlenet_layers(aux), K=128, dtype="f32",
+    lr 0.08 (Sec. 7.3 "Ultra-deep models"), mu 0.9, wd 2e-4 (Sec. 7.1).
+    caffe_bias: every bias segment takes twice the learning rate and no
+    weight decay (lr_mult 2, decay_mult 0), as in the Caffe network
+    definitions the paper trains with (Sec. 7.1 item 2)."""
+    name = "googlenet" + ("_aux" if aux else "") + ("_caffe_bias" if caffe_bias else "")
+    return _make(name, googlenet_layers(aux), caffe_bias_mults=caffe_bias, K=128, dtype="f32",
                  batch=1024, lr=0.08, mu=0.9, wd=2e-4, grad_std="fan_in", weight_init="xavier_bias0.2")
 
 
@@ -203,9 +207,14 @@ def alexnet(grouped=True):
 WORKLOADS = {"flat": flat, "nin": nin, "googlenet": googlenet, "vgg19": vgg19, "alexnet": alexnet}
 
 
+VARIANTS = ("googlenet_aux", "googlenet_caffe_bias", "alexnet_ungrouped")
+
+
 def get(name):
     if name == "googlenet_aux":
         return googlenet(aux=True)
+    if name == "googlenet_caffe_bias":
+        return googlenet(caffe_bias=True)
     if name == "alexnet_ungrouped":
         return alexnet(grouped=False)
     return WORKLOADS[name]()
