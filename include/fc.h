@@ -104,15 +104,16 @@ typedef struct fc_plan fc_plan;
  *   because HBM serves a replica stream with one write stream better than
  *   with two).
  * RESIDENT: one persistent launch, one block of 16 waves per compute unit;
- *   each block first reduces its share of the parameters into LDS (HBM sees a
- *   pure read stream) and then updates them from LDS, so the raw sum never
- *   goes to HBM.  A block's share per round is what fits one compute unit's
- *   LDS (1 KiB per 256-element tile: about 10 M parameters per round over 256
- *   compute units of 160 KiB); larger plans take several rounds, one launch
- *   per round.  It also
- *   makes fc_tree_reduce store the sums only after each read phase.  Tiles of
- *   64 lanes x 1 vector with batches of 16 replicas (default), or x 2 vectors
- *   with batches of 4 (vecs_per_thread 2, K < 512).
+ *   each block first reduces its share of the parameters on chip (HBM sees a
+ *   pure read stream) and then updates them from there, so the raw sum never
+ *   goes to HBM.  A block's share per round is what one compute unit holds:
+ *   its LDS (1 KiB per 256-element tile: about 10 M parameters per round over
+ *   256 compute units of 160 KiB), plus, for fp32 replicas with K < 32, the
+ *   tiles its waves keep in registers (as much again with 1 vector per lane,
+ *   0.8x with 2); larger plans take several rounds, one launch per round.  It
+ *   also makes fc_tree_reduce store the sums only after each read phase.
+ *   Tiles of 64 lanes x 1 vector with batches of 16 replicas (default), or x 2
+ *   vectors with batches of 4 (vecs_per_thread 2, K < 512).
  * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
  *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
  *   round holds the plan or a parameter's replicas take at least 48 bytes

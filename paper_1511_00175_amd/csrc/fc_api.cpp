@@ -43,6 +43,7 @@ struct fc_plan {
     int res_rounds = 0;
     int res_lds = 0;                 // RESIDENT: LDS bytes per block
     int res_slot = 0;                // RESIDENT: LDS bytes per tile
+    int res_in_regs = 0;             // RESIDENT: tiles per block held in registers
     bool res_record = false;         // RESIDENT: launches record per-block rates into d_clock
     std::vector<int> res_ranges;     // RESIDENT: host copy of the d_ranges table
     unsigned long long* d_clock = nullptr;  // RESIDENT: per block, the kernel's phase-1 clock and XCD
@@ -402,18 +403,23 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     for (int j = 0; j < nseg; ++j)
         res_tiles += (segs[j].length / vec + tile_vecs_r - 1) / tile_vecs_r + (segs[j].length % vec ? 1 : 0);
     const uint64_t slot_bytes = fc::RESIDENT_SLOT * sizeof(float) * res_u;
-    const uint64_t cap = std::max<uint64_t>(1, static_cast<uint64_t>(std::max(lds_cu, 0)) / slot_bytes);
+    const uint64_t cap_lds = std::max<uint64_t>(1, static_cast<uint64_t>(std::max(lds_cu, 0)) / slot_bytes);
+    // a block's tiles in one round: the waves' register-held tiles first,
+    // then LDS slots
+    const int res_rt = fc::resident_rtiles(gdt, res_u, res_c, bit_length(K / res_c));
+    const uint64_t in_regs = static_cast<uint64_t>(fc::RESIDENT_WAVES) * res_rt;
+    const uint64_t cap = cap_lds + in_regs;
     int res_grid = std::max(1, cus);
     if (opts && opts->max_blocks > 0) res_grid = std::min(res_grid, opts->max_blocks);
     if (res_tiles > 0 && res_tiles < static_cast<uint64_t>(res_grid)) res_grid = static_cast<int>(res_tiles);
     const uint64_t res_rounds = std::max<uint64_t>(1, (res_tiles + res_grid * cap - 1) / (res_grid * cap));
     const uint64_t res_ranges = static_cast<uint64_t>(res_grid) * res_rounds;
-    // LDS for the most tiles a block may ever hold, so that rebalanced
-    // ranges (fc_plan_balance) never need more than a launch already has,
-    // also in a captured graph (measured on MI355X: the size itself does
-    // not change the speed)
-    const uint64_t res_lds =
-        std::min<uint64_t>(cap, std::max<uint64_t>(1, (res_tiles + res_rounds - 1) / res_rounds)) * slot_bytes;
+    // LDS for the most tiles a block may ever hold beyond its registers, so
+    // that rebalanced ranges (fc_plan_balance) never need more than a launch
+    // already has, also in a captured graph (measured on MI355X: the size
+    // itself does not change the speed)
+    const uint64_t most = std::min<uint64_t>(cap, std::max<uint64_t>(1, (res_tiles + res_rounds - 1) / res_rounds));
+    const uint64_t res_lds = std::max<uint64_t>(1, most > in_regs ? most - in_regs : 0) * slot_bytes;
     if (res_ranges > static_cast<uint64_t>(INT32_MAX) - 1) return FC_EINVAL;
     // algorithmic bytes of one step (saturating)
     const uint64_t per_elem = static_cast<uint64_t>(K) * (gdt == FC_F16 ? 2 : 4) + 16;
@@ -426,6 +432,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         sh.block = 64;
         sh.vecs = res_u;
         sh.kchunk = res_c;
+        sh.rtiles = res_rt;
     }
 
     fc_plan* p = new (std::nothrow) fc_plan();
@@ -500,6 +507,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         p->res_rounds = static_cast<int>(res_rounds);
         p->res_lds = static_cast<int>(res_lds);
         p->res_slot = static_cast<int>(slot_bytes);
+        p->res_in_regs = static_cast<int>(in_regs);
         p->res_record = (res_tiles + res_ranges - 1) / res_ranges >= static_cast<uint64_t>(fc::RESIDENT_RECORD_MIN_TILES);
         try {
             ranges.resize(static_cast<size_t>(res_ranges) + 1);
@@ -628,7 +636,7 @@ static int fc_plan_balance_body(fc_plan* p, void* stream, float* xcd_rate, int n
     // every block's tiles fit its LDS; equal shares always fit
     for (int b = 0; b < G; ++b) rel_b[b] = rel[xcd[b]];
     try {
-        (void)fc::balanced_ranges(p->ntiles, R, G, rel_b, p->res_lds / p->res_slot, ranges);
+        (void)fc::balanced_ranges(p->ntiles, R, G, rel_b, p->res_lds / p->res_slot + p->res_in_regs, ranges);
     } catch (const std::bad_alloc&) {
         return FC_ENOMEM;
     }
@@ -784,6 +792,7 @@ static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, vo
         rc = launch(p, FC_KERNEL_BCAST, s, [&] {
             if (p->schedule != FC_SCHED_RESIDENT) return fc::launch_bcast(p->shape, p->grid, a, s);
             // resident plans: the step's ranges, one launch per round
+            a.slots = p->res_lds / p->res_slot;
             for (int round = 0; round < p->res_rounds; ++round) {
                 a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
                 const hipError_t e =

@@ -191,6 +191,11 @@ template <int V> __device__ __forceinline__ void st32r(gptr_w_t base, uint32_t o
     if constexpr (V == 1) {
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x[0]), rsrc((const void*)base), off, 0,
                                               CPOL_RESULT_STORE);
+    } else if constexpr (V == 2) {
+        f2 t;
+        t.x = x[0]; t.y = x[1];
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2, t), rsrc((const void*)base), off, 0,
+                                              CPOL_RESULT_STORE);
     } else {
 #pragma unroll
         for (int q = 0; q < V / 4; ++q) {
@@ -207,6 +212,10 @@ template <int V> __device__ __forceinline__ void ld32s(gptr_t base, uint32_t off
     if constexpr (V == 1) {
         x[0] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rsrc((const void*)base), off, 0,
                                                                             CPOL_STREAM_LOAD));
+    } else if constexpr (V == 2) {
+        const f2 t = __builtin_bit_cast(f2, __builtin_amdgcn_raw_buffer_load_b64(rsrc((const void*)base), off, 0,
+                                                                                CPOL_STREAM_LOAD));
+        x[0] = t.x; x[1] = t.y;
     } else {
 #pragma unroll
         for (int q = 0; q < V / 4; ++q) {
@@ -512,15 +521,18 @@ __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uin
 // so that each destination receives the block's whole range as one contiguous
 // run (measured on MI355X: 3-4% faster than storing all K copies of a tile
 // before the next tile).  Wave q stores the tiles whose slots it filled, so
-// it reads back only what it wrote itself.  Every wave of the block calls it.
-template <int W, int U>
+// it reads back only what it wrote itself.  Before its slots, each wave calls
+// extra(d) with the destination, to store values it holds in registers.
+// Every wave of the block calls it.
+template <int W, int U, class Extra>
 __device__ __forceinline__ void store_slots(const Tile* tiles, float* const* dst, int K, const float* slots, int lo,
-                                            int hi) {
+                                            int hi, Extra&& extra) {
     constexpr int SLOT = RESIDENT_SLOT * U;
     const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const uint32_t lane = threadIdx.x & 63;
     for (int k = 0; k < K; ++k) {
         const gptr_w_t d = gwrite(ldc(dst, k));
+        extra(d);
         for (int j = q; j < hi - lo; j += W) {
             const Tile tile = ld_tile(tiles, lo + j);
             const float* slot = slots + j * SLOT;
@@ -539,29 +551,109 @@ __device__ __forceinline__ void store_slots(const Tile* tiles, float* const* dst
     }
 }
 
+// Phase 1 of the resident kernel on one tile: the raw sums of the lane's
+// elements in x.  fp32 replicas (DT = FC_F32_PAIRS): the lane's values of the
+// tile's elements [256 u, 256 u + 256) are the pairs at 256 u + 2 lane and
+// 256 u + 128 + 2 lane (x.a[u][0..1] and x.a[u][2..3]); fp16: the lane's
+// vector u is tile vector lane + 64 u.  A pair or vector past the tile's
+// elements re-reads the first one.  Tail tile: the lane's element in x.a[0][0].
+template <int DT, int U, int C, int MAXD, bool TREE>
+__device__ __forceinline__ void reduce_tile(const ReduceArgs& a, const Tile& tile, uint32_t lane, Acc<U, 4>& x) {
+    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
+    if (!(tile.seg & TAIL_BIT)) {
+        if constexpr (DT == FC_F32_PAIRS) {
+            const uint32_t ne = tile.count * 4;
+            OffPair off[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                off[u].a = (e0 < ne ? e0 : 0u) * 4;
+                off[u].b = (e1 < ne ? e1 : 0u) * 4;
+            }
+            reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * 4, off, x);
+        } else {
+            uint32_t off[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t vi = lane + 64 * u;
+                off[u] = (vi < tile.count ? vi : 0u) * 4 * SG;
+            }
+            reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
+        }
+    } else {
+        const uint32_t vi = lane < tile.count ? lane : 0u;
+        const uint32_t off[1] = {vi * SG};
+        Acc<1, 1> y;
+        reduce<DT, 1, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, y);
+        x.a[0][0] = y.a[0][0];
+    }
+}
+
+// Phases 2 and 3 for a tile whose raw sums a wave kept in registers (x, in
+// reduce_tile's fp32-pair layout): finish the lane's pairs (the update of w
+// and v, or the store of the sum), leaving w' in x for the broadcast; and the
+// store of w' to one destination d.
+template <int U, int MODE>
+__device__ __forceinline__ void finish_kept(const ReduceArgs& a, const Tile& tile, uint32_t lane, float lr_j,
+                                            float wd_j, Acc<U, 4>& x) {
+    const uint64_t start4 = tile.start * 4;
+    if (!(tile.seg & TAIL_BIT)) {
+        const uint32_t ne = tile.count * 4;  // a multiple of 4: pairs are never split
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+            if (e0 < ne) finish<2, MODE, true>(a, start4, e0 * 4, &x.a[u][0], lr_j, wd_j, &x.a[u][0]);
+            if (e1 < ne) finish<2, MODE, true>(a, start4, e1 * 4, &x.a[u][2], lr_j, wd_j, &x.a[u][2]);
+        }
+    } else if (lane < tile.count) {
+        finish<1, MODE, true>(a, start4, lane * 4, &x.a[0][0], lr_j, wd_j, &x.a[0][0]);
+    }
+}
+
+template <int U>
+__device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_t lane, const Acc<U, 4>& x) {
+    const uint64_t start4 = tile.start * 4;
+    if (!(tile.seg & TAIL_BIT)) {
+        const uint32_t ne = tile.count * 4;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+            if (e0 < ne) st32r<2>(d + start4, e0 * 4, &x.a[u][0]);
+            if (e1 < ne) st32r<2>(d + start4, e1 * 4, &x.a[u][2]);
+        }
+    } else if (lane < tile.count) {
+        st32r<1>(d + start4, lane * 4, &x.a[0][0]);
+    }
+}
+
 // ------------------------------------------------------------------ resident step
 // One persistent block per CU, for each of the plan's rounds.  Phase 1: wave
 // q of the block reduces tiles lo + q, lo + q + W, ... of its range in the
 // same association as reduce_kernel (fp32 replicas read as 8-byte pairs,
-// DT = FC_F32_PAIRS) and parks the raw sums in the tile's LDS slot in element
+// DT = FC_F32_PAIRS) and keeps each tile's raw sums on chip: the wave's
+// first RT tiles in registers, the others in the tile's LDS slot in element
 // order; HBM sees a pure read stream, no writes.  Phase 2, after a barrier:
-// wave q finishes the same tiles from LDS (the SGD update, or the store of
-// the raw sum); with a broadcast, phase 3 stores w' to the K copies one
-// destination at a time (store_slots).  In round r the blocks' ranges are neighbours,
-// so the whole grid streams one region of the parameters at a time.  Blocks
-// share nothing, so the result does not depend on how many of them are
-// resident at once, nor on how the ranges divide the tiles.  Each block
-// records how long its phase 1 took and on which XCD: blocks on some XCDs
-// read more slowly than on others (measured on MI355X: 6-10%), and the host
-// can give each block a share of tiles in proportion to its XCD's rate.
-template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE>
+// wave q finishes the same tiles (the SGD update, or the store of the raw
+// sum), from its registers and from LDS; with a broadcast, phase 3 stores w'
+// to the K copies one destination at a time (store_slots).  The registers
+// multiply what one round holds: LDS holds 160 KiB per CU, and RT tiles of
+// 64 lanes x U vectors per wave add 16 * RT * U KiB.  In round r the blocks'
+// ranges are neighbours, so the whole grid streams one region of the
+// parameters at a time.  Blocks share nothing, so the result does not depend
+// on how many of them are resident at once, nor on how the ranges divide the
+// tiles.  Each block records how long its phase 1 took and on which XCD:
+// blocks on some XCDs read more slowly than on others (measured on MI355X:
+// 6-10%), and the host can give each block a share of tiles in proportion to
+// its XCD's rate.
+template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE, int RT>
 __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
+    static_assert(RT == 0 || DT == FC_F32_PAIRS, "register-held tiles keep the fp32 pair layout");
     // 16-byte aligned, so that a lane's 4 sums move as one 16-byte LDS access
     extern __shared__ f4 slot_vecs[];
     float* slots = reinterpret_cast<float*>(slot_vecs);
     const ReduceArgs& a = ra.r;
-    constexpr uint32_t SG = DT == FC_F16 ? 2 : 4;
     constexpr int SLOT = RESIDENT_SLOT * U;  // floats of LDS per tile of 64 * U vectors
+    constexpr int NKEEP = RT > 0 ? RT : 1;
     const int q = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const uint32_t lane = threadIdx.x & 63;
     for (int round = 0; round < ra.rounds; ++round) {
@@ -569,53 +661,36 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
         const int b = static_cast<int>(blockIdx.x) + round * static_cast<int>(gridDim.x);
         const int lo = ldc(ra.ranges, b);
         const int hi = ldc(ra.ranges, b + 1);
-        for (int t = lo + q; t < hi; t += W) {
+        const int lo_lds = lo + W * RT;  // tile lo_lds + j sits in LDS slot j
+        // phase 1: tiles lo + q + W i with i < RT into registers ...
+        Acc<U, 4> kept[NKEEP];
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+            const int t = lo + q + W * i;
+            if (t < hi) reduce_tile<DT, U, C, MAXD, TREE>(a, ld_tile(a.tiles, t), lane, kept[i]);
+        }
+        // ... the others into LDS, in element order
+        for (int t = lo_lds + q; t < hi; t += W) {
             const Tile tile = ld_tile(a.tiles, t);
-            float* slot = slots + (t - lo) * SLOT;
-            if (!(tile.seg & TAIL_BIT)) {
-                if constexpr (DT == FC_F32_PAIRS) {
-                    // the lane's values of the tile's elements [256 u, 256 u + 256): the
-                    // pairs at 256 u + 2 lane and 256 u + 128 + 2 lane; a pair past the
-                    // tile's elements re-reads pair 0
-                    const uint32_t ne = tile.count * 4;
-                    OffPair off[U];
+            float* slot = slots + (t - lo_lds) * SLOT;
+            Acc<U, 4> x;
+            reduce_tile<DT, U, C, MAXD, TREE>(a, tile, lane, x);
+            if (tile.seg & TAIL_BIT) {
+                slot[lane] = x.a[0][0];
+            } else if constexpr (DT == FC_F32_PAIRS) {
 #pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-                        off[u].a = (e0 < ne ? e0 : 0u) * 4;
-                        off[u].b = (e1 < ne ? e1 : 0u) * 4;
-                    }
-                    Acc<U, 4> x;
-                    reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * 4, off, x);
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-                        slot[e0] = x.a[u][0];
-                        slot[e0 + 1] = x.a[u][1];
-                        slot[e1] = x.a[u][2];
-                        slot[e1 + 1] = x.a[u][3];
-                    }
-                } else {
-                    // vector u of the lane is tile vector lane + 64 u; idle lanes re-read vector 0
-                    uint32_t off[U];
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const uint32_t vi = lane + 64 * u;
-                        off[u] = (vi < tile.count ? vi : 0u) * 4 * SG;
-                    }
-                    Acc<U, 4> x;
-                    reduce<DT, 4, U, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
-#pragma unroll
-                    for (int u = 0; u < U; ++u)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) slot[(lane + 64 * u) * 4 + i] = x.a[u][i];
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                    slot[e0] = x.a[u][0];
+                    slot[e0 + 1] = x.a[u][1];
+                    slot[e1] = x.a[u][2];
+                    slot[e1 + 1] = x.a[u][3];
                 }
             } else {
-                const uint32_t vi = lane < tile.count ? lane : 0u;
-                const uint32_t off[1] = {vi * SG};
-                Acc<1, 1> x;
-                reduce<DT, 1, 1, C, MAXD, TREE>(a.grads, a.K, tile.start * SG, off, x);
-                slot[lane] = x.a[0][0];
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) slot[(lane + 64 * u) * 4 + i] = x.a[u][i];
             }
         }
         __syncthreads();
@@ -630,10 +705,26 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
                                    __HIP_MEMORY_SCOPE_AGENT);
             c[2] = static_cast<unsigned long long>(__builtin_amdgcn_s_getreg((3 << 11) | 20));
         }
-        const int n = (hi - lo) * 64;
+        // phase 2: the register-held tiles ...
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+            const int t = lo + q + W * i;
+            if (t < hi) {
+                const Tile tile = ld_tile(a.tiles, t);
+                float lr_j = 0.0f, wd_j = 0.0f;
+                if constexpr (MODE == MODE_STEP) {
+                    const int sj = static_cast<int>(tile.seg & SEG_MASK);
+                    lr_j = a.lr * ldc(a.mults, 2 * sj);
+                    wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
+                }
+                finish_kept<U, MODE>(a, tile, lane, lr_j, wd_j, kept[i]);
+            }
+        }
+        // ... then those in LDS, one tile per wave
+        const int n = hi > lo_lds ? (hi - lo_lds) * 64 : 0;
         for (int e = static_cast<int>(threadIdx.x); e < n; e += 64 * W) {
-            const int j = __builtin_amdgcn_readfirstlane(e / 64);  // one tile per wave
-            const Tile tile = ld_tile(a.tiles, lo + j);
+            const int j = __builtin_amdgcn_readfirstlane(e / 64);
+            const Tile tile = ld_tile(a.tiles, lo_lds + j);
             float lr_j = 0.0f, wd_j = 0.0f;
             if constexpr (MODE == MODE_STEP) {
                 const int sj = static_cast<int>(tile.seg & SEG_MASK);
@@ -654,8 +745,15 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
             }
         }
         if constexpr (MODE == MODE_STEP) {
-            // phase 3, the broadcast: w' now sits in the slots
-            if (a.dst) store_slots<W, U>(a.tiles, a.dst, a.K, slots, lo, hi);
+            // phase 3, the broadcast: w' now sits in the registers and slots
+            if (a.dst)
+                store_slots<W, U>(a.tiles, a.dst, a.K, slots, lo_lds, hi > lo_lds ? hi : lo_lds, [&](gptr_w_t d) {
+#pragma unroll
+                    for (int i = 0; i < RT; ++i) {
+                        const int t = lo + q + W * i;
+                        if (t < hi) store_kept<U>(d, ld_tile(a.tiles, t), lane, kept[i]);
+                    }
+                });
         }
         __syncthreads();  // the next round's phase 1 overwrites the slots
     }
@@ -725,10 +823,11 @@ __global__ __launch_bounds__(256) void bcast_kernel(BcastArgs a) {
 }
 
 // Broadcast on a plan with the resident schedule: one persistent block of W
-// waves per CU takes its range of the round's tiles (a.ranges), its waves
-// copy the source values of those tiles into LDS slots (wave q the tiles
-// lo + q, lo + q + W, ...), and the block stores them to the K destinations
-// one destination at a time (store_slots).
+// waves per CU takes its range of the round's tiles (a.ranges) in pieces of
+// at most a.slots tiles (the LDS it has), its waves copy the source values of
+// a piece into LDS slots (wave q the tiles lo + q, lo + q + W, ...), and the
+// block stores them to the K destinations one destination at a time
+// (store_slots, whose last barrier frees the slots for the next piece).
 template <int W, int U>
 __global__ __launch_bounds__(64 * W) void resident_bcast_kernel(BcastArgs a) {
     extern __shared__ f4 slot_vecs[];
@@ -738,21 +837,24 @@ __global__ __launch_bounds__(64 * W) void resident_bcast_kernel(BcastArgs a) {
     const uint32_t lane = threadIdx.x & 63;
     const int lo = ldc(a.ranges, blockIdx.x);
     const int hi = ldc(a.ranges, blockIdx.x + 1);
-    for (int t = lo + q; t < hi; t += W) {
-        const Tile tile = ld_tile(a.tiles, t);
-        float* slot = slots + (t - lo) * SLOT;
-        const uint64_t start4 = tile.start * 4;
-        if (!(tile.seg & TAIL_BIT)) {
+    for (int p0 = lo; p0 < hi; p0 += a.slots) {
+        const int p1 = hi - p0 < a.slots ? hi : p0 + a.slots;
+        for (int t = p0 + q; t < p1; t += W) {
+            const Tile tile = ld_tile(a.tiles, t);
+            float* slot = slots + (t - p0) * SLOT;
+            const uint64_t start4 = tile.start * 4;
+            if (!(tile.seg & TAIL_BIT)) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t vi = lane + 64 * u;
-                if (vi < tile.count) ld32s<4>(gread(a.src) + start4, vi * 16, slot + vi * 4);
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t vi = lane + 64 * u;
+                    if (vi < tile.count) ld32s<4>(gread(a.src) + start4, vi * 16, slot + vi * 4);
+                }
+            } else if (lane < tile.count) {
+                ld32s<1>(gread(a.src) + start4, lane * 4, slot + lane);
             }
-        } else if (lane < tile.count) {
-            ld32s<1>(gread(a.src) + start4, lane * 4, slot + lane);
         }
+        store_slots<W, U>(a.tiles, a.dst, a.K, slots, p0, p1, [](gptr_w_t) {});
     }
-    store_slots<W, U>(a.tiles, a.dst, a.K, slots, lo, hi);
 }
 
 // ------------------------------------------------------------------ dispatch
@@ -803,22 +905,35 @@ hipError_t launch_reduce_dt(const Shape& sh, int mode, int grid, const ReduceArg
 }
 
 // The resident kernel instance for a plan's shape: f(kernel instance tag).
+// The register-held tiles per wave (sh.rtiles) are the plan's
+// (resident_rtiles): its rounds are sized for them.
 template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F&& f) {
     if (sh.block != 64) return hipErrorInvalidValue;
-    auto go = [&](auto u, auto c) {
+    auto go = [&](auto u, auto c, auto d, auto rt) {
         return pick<MODE_REDUCE, MODE_STEP>(mode, [&](auto md) {
-            auto at = [&](auto d) {
-                if (sh.tree) return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, true, md.value>);
-                return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, false, md.value>);
-            };
-            if constexpr (u.value == 1) return pick_maxd(sh.maxd, at);
-            else return sh.maxd <= 5 ? at(I<5>{}) : at(I<7>{});
+            if (sh.tree)
+                return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, true, md.value, rt.value>);
+            return f(&resident_kernel<DT, RESIDENT_WAVES, u.value, c.value, d.value, false, md.value, rt.value>);
         });
     };
+    constexpr bool pairs = DT == FC_F32_PAIRS;
     // (lane vectors, replicas per batch) of the resident tiles; two vectors
     // per lane only with stacks up to depth 7 (deeper ones would spill)
-    if (sh.vecs == 1 && sh.kchunk == 16) return go(I<1>{}, I<16>{});
-    if (sh.vecs == 2 && sh.kchunk == 4 && sh.maxd <= 7) return go(I<2>{}, I<4>{});
+    if (sh.vecs == 1 && sh.kchunk == 16) {
+        if constexpr (pairs) {
+            if (sh.rtiles == 10 && sh.maxd <= 1) return go(I<1>{}, I<16>{}, I<1>{}, I<10>{});
+        }
+        if (sh.rtiles != 0) return hipErrorInvalidValue;
+        return pick_maxd(sh.maxd, [&](auto d) { return go(I<1>{}, I<16>{}, d, I<0>{}); });
+    }
+    if (sh.vecs == 2 && sh.kchunk == 4) {
+        if constexpr (pairs) {
+            if (sh.rtiles == 4 && sh.maxd <= 3) return go(I<2>{}, I<4>{}, I<3>{}, I<4>{});
+        }
+        if (sh.rtiles != 0) return hipErrorInvalidValue;
+        if (sh.maxd <= 5) return go(I<2>{}, I<4>{}, I<5>{}, I<0>{});
+        if (sh.maxd <= 7) return go(I<2>{}, I<4>{}, I<7>{}, I<0>{});
+    }
     return hipErrorInvalidValue;
 }
 

@@ -33,6 +33,7 @@ struct Shape {
     int vecs;         // 4-element lane-vectors per thread (1, 2 or 4)
     int kchunk;       // replicas loaded per batch (2, 4, 8 or 16; see the pairs compiled)
     int maxd;         // depth of the pending-subtree stack (>= bit length of K / kchunk)
+    int rtiles;       // resident kernel: tiles per wave whose raw sums stay in registers
 };
 
 struct ReduceArgs {
@@ -87,6 +88,7 @@ struct BcastArgs {
     float* const* dst;
     int K;
     const int* ranges;            // resident plans: gridDim.x + 1 tile indices of one round
+    int slots;                    // resident plans: LDS tile slots per block (>= 1)
 };
 
 // Largest pending-subtree stack depth compiled (stack depths 5, 7 and 10 are

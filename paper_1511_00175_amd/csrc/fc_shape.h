@@ -50,6 +50,21 @@ inline void default_resident_shape(fc_dtype gdt, int K, int& u, int& c) {
 }
 inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128; }
 
+// Tiles per wave whose raw sums the resident kernel keeps in registers, on
+// top of the LDS slots: what a wave's 128 VGPRs (4 waves per SIMD) leave
+// beside phase 1 when the tree's pending-subtree stack is shallow, for fp32
+// replicas (the compiler's resource report, fp32 tree step: 1 vector and
+// batches of 16 with a depth-1 stack (K < 32) holds 10 tiles in 128 VGPRs,
+// 2 vectors and batches of 4 with a depth-3 stack (K < 32) holds 4 in 123;
+// none spills).  16 waves x 10 tiles of 1 KiB add 160 KiB per CU, 16 x 4 of
+// 2 KiB add 128 KiB: a round holds 2x or 1.8x the parameters of LDS alone.
+inline int resident_rtiles(int gdt, int u, int c, int maxd) {
+    if (gdt != FC_F32) return 0;
+    if (u == 1 && c == 16 && maxd <= 1) return 10;
+    if (u == 2 && c == 4 && maxd <= 3) return 4;
+    return 0;
+}
+
 inline bool compiled_pair(int u, int c) {
     return (u == 1 && (c == 8 || c == 16)) || (u == 2 && (c == 8 || c == 16)) ||
            (u == 4 && (c == 2 || c == 4 || c == 8));

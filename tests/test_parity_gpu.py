@@ -163,18 +163,22 @@ def test_schedule_resolution(fc):
         if dtype == "f32" and K <= 16:
             # tiles of 2 vectors per lane, batches of 4: 2 tiles of 512 elements
             # (the second of 488), then the 5-element segment's vector and its
-            # tail tile; LDS for the 4 tiles a block could be given, 2 KiB each
+            # tail tile; the 4 tiles a block could be given fit its waves'
+            # registers (4 tiles each), so LDS keeps its one-slot minimum, 2 KiB
             assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 2, 4, 1)
-            assert (info.ntiles, info.grid, info.lds_bytes) == (4, 4, 4 * 2048)
+            assert (info.ntiles, info.grid, info.lds_bytes) == (4, 4, 2048)
         else:
             assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
             # 3 tiles of 256 elements and one of 232, then the 5-element segment's
             # vector and its tail tile: one tile per block; LDS for the 6 tiles a
-            # block could be given (fc_plan_balance), 1 KiB each
-            assert (info.ntiles, info.grid, info.lds_bytes) == (6, 6, 6 * 1024)
-    # 160 tiles per block fill 160 KiB of LDS: 256-element tiles for cus * 160 tiles fit
-    fits = [(0, cus * 160 * 256, 1, 1)]
-    big = [(0, cus * 160 * 256 + 4, 1, 1)]
+            # block could be given (fc_plan_balance), 1 KiB each -- one slot
+            # for fp32 with K < 32, whose waves hold 10 tiles each in registers
+            assert (info.ntiles, info.grid) == (6, 6)
+            assert info.lds_bytes == (1024 if dtype == "f32" and K < 32 else 6 * 1024), (K, dtype)
+    # fp32 K=8: tiles of 512 elements, 144 per block and round (80 in 160 KiB
+    # of LDS, 4 in the registers of each of the 16 waves)
+    fits = [(0, cus * 144 * 512, 1, 1)]
+    big = [(0, cus * 144 * 512 + 4, 1, 1)]
     info = fc.Plan(fits, 8, "f32", "tree").info()
     assert (info.schedule, info.rounds, info.lds_bytes, info.grid) == (3, 1, 160 * 1024, cus)
     for K, dtype, two in ((64, "f32", False), (65, "f32", True), (128, "f16", False), (129, "f16", True)):
@@ -197,6 +201,13 @@ def test_schedule_resolution(fc):
     assert fc.Plan(big, 64, "f32", "tree", block_threads=64).info().schedule == 1
     assert fc.Plan(big, 65, "f32", "tree", block_threads=64).info().schedule == 2
     info = fc.Plan(big, 8, "f32", "tree", schedule=3).info()
+    assert (info.schedule, info.rounds, info.lds_bytes) == (3, 2, 160 * 1024)
+    # 1 vector and batches of 16 (fp32, 16 < K < 32): 320 tiles of 256 per
+    # block and round (160 in LDS, 10 per wave in registers)
+    one = [(0, cus * 320 * 256, 1, 1)]
+    info = fc.Plan(one, 20, "f32", "tree").info()
+    assert (info.schedule, info.rounds, info.lds_bytes, info.vecs_per_thread) == (3, 1, 160 * 1024, 1)
+    info = fc.Plan([(0, cus * 320 * 256 + 4, 1, 1)], 20, "f32", "tree").info()
     assert (info.schedule, info.rounds, info.lds_bytes) == (3, 2, 160 * 1024)
 
 
@@ -261,7 +272,7 @@ def test_broadcast_matches_oracle(fc, K, schedule, max_blocks, vecs, dtype):
     every segment element (special values included) and keeps its fill
     value elsewhere; the replica type only changes the plan's tile map."""
     import torch
-    segs = table(15000 + K, dtype, nseg=8, max_len=30000)  # 124-177 K elements: 485+ tiles of 256
+    segs = table(15000 + K, dtype, nseg=8, max_len=60000)  # 248-354 K elements: 970+ tiles of 256
     n = alloc_len(segs)
     rng = np.random.default_rng(K * 31 + schedule * 7 + max_blocks)
     src = host_replicas(rng, 1, n, np.float32, special=True)[0]
@@ -471,7 +482,8 @@ def test_resident_plans_with_different_lds_interleave(fc):
     rng = np.random.default_rng(77)
     big = fc.Plan(rows_big, K, "f32", "tree", schedule=3)
     small = fc.Plan(rows_small, K, "f32", "tree", schedule=3)
-    assert big.info().lds_bytes == 160 * 1024 and small.info().lds_bytes == 12 * 1024
+    # 6 tiles of 512 fit the small plan's registers: one LDS slot
+    assert big.info().lds_bytes == 160 * 1024 and small.info().lds_bytes == 2 * 1024
     reps = torch.from_numpy(rng.standard_normal((K, big_n), dtype=np.float32)).cuda()
     out = torch.full((big_n,), -1.0, device="cuda")
     big.tree_reduce(reps, out)
@@ -498,15 +510,18 @@ def test_batch_not_a_power_of_two(fc, batch):
 
 
 @pytest.mark.parametrize("n,K,max_blocks,vecs", [(1000, 4, 0, 1), (5_000_000, 8, 0, 1), (40_000_000, 8, 0, 1),
-                                                 (143_667_240, 16, 0, 1), (60_965_224, 128, 0, 2),
-                                                 (300_000, 8, 3, 1), (1, 1, 0, 1)])
+                                                 (143_667_240, 16, 0, 1), (143_667_240, 16, 0, 2),
+                                                 (60_965_224, 128, 0, 2), (60_965_224, 32, 0, 1),
+                                                 (300_000, 8, 3, 1), (300_000, 8, 3, 2), (1, 1, 0, 1)])
 def test_resident_partition(fc, n, K, max_blocks, vecs):
     """The resident plan's grid, rounds and LDS per block follow from the tile
-    count and the CU's LDS: rounds = ceil(tiles / (grid * slots)) for tiles of
-    64 * vecs vectors, each with 1 KiB * vecs of LDS (160 KiB per CU); a
+    count, the CU's LDS and the tiles its waves hold in registers: rounds =
+    ceil(tiles / (grid * (slots + 16 * rt))) for tiles of 64 * vecs vectors,
+    each with 1 KiB * vecs of LDS (160 KiB per CU), rt = 10 (1 vector) or 4
+    (2 vectors) register-held tiles per wave for fp32 with K < 32, else 0; a
     block's LDS holds the slots of as many tiles as it could be given in one
-    round (a round's tiles, at most the CU's slots), so that rebalanced
-    ranges never need more."""
+    round beyond its registers (a round's tiles, at most the CU's capacity),
+    so that rebalanced ranges never need more."""
     import math
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -517,8 +532,9 @@ def test_resident_partition(fc, n, K, max_blocks, vecs):
     grid = min(cus, max_blocks) if max_blocks else cus
     grid = min(grid, tiles)
     slots = (160 * 1024) // (1024 * vecs)
-    rounds = max(1, math.ceil(tiles / (grid * slots)))
-    per = min(slots, max(1, math.ceil(tiles / rounds)))
+    regs = 16 * ((10 if vecs == 1 else 4) if K < 32 else 0)
+    rounds = max(1, math.ceil(tiles / (grid * (slots + regs))))
+    per = max(1, min(slots + regs, max(1, math.ceil(tiles / rounds))) - regs)
     assert (info.ntiles, info.grid, info.rounds, info.lds_bytes) == (tiles, grid, rounds, per * 1024 * vecs), \
         (info.ntiles, info.grid, info.rounds, info.lds_bytes)
     assert info.lds_bytes <= 160 * 1024
@@ -686,6 +702,7 @@ def test_graph_replays_broadcast(fc):
     gives every destination the oracle's copy of the source and of w'."""
     import torch
     segs = table(19000, "f32", nseg=6, max_len=20000)
+    segs = segs + [(alloc_len(segs), 100000, 1.0, 1.0)]  # > 144 tiles of 512: several rounds
     K = 5
     n = alloc_len(segs)
     rng = np.random.default_rng(13)
@@ -831,23 +848,64 @@ def test_balance_drains_the_plans_stream(fc):
     p.close()
 
 
-def test_balance_with_full_lds_keeps_equal_shares(fc):
-    """Two blocks whose equal share of each round already fills all 160 LDS
-    slots (640 tiles, 2 rounds): no unequal division fits, so the shares
-    fc_plan_balance writes stay equal (160 and 160); the steps after it stay
-    bit-exact."""
-    n = 2 * 2 * 160 * 256
+@pytest.mark.parametrize("K,per_block", [(40, 160), (6, 320)])
+def test_balance_with_full_lds_keeps_equal_shares(fc, K, per_block):
+    """Two blocks whose equal share of each round already fills the block
+    (2 rounds: K=40, 160 LDS slots; K=6, 160 slots and 160 tiles in its
+    waves' registers): no unequal division fits, so the shares fc_plan_balance
+    writes stay equal; the steps after it stay bit-exact."""
+    n = 2 * 2 * per_block * 256
     segs = [(0, n, 1.0, 1.0)]
     opts = dict(schedule=3, max_blocks=2, vecs_per_thread=1)
-    p = fc.Plan(segs, 6, "f32", "tree", **opts)
+    p = fc.Plan(segs, K, "f32", "tree", **opts)
     info = p.info()
     p.close()
-    assert (info.ntiles, info.rounds, info.lds_bytes) == (640, 2, 160 * 1024)
+    assert (info.ntiles, info.rounds, info.lds_bytes) == (4 * per_block, 2, 160 * 1024)
     rates = []
-    bad = run_steps(fc, segs, 6, "f32", "tree", np.random.default_rng(21), steps=3, opts=opts,
+    bad = run_steps(fc, segs, K, "f32", "tree", np.random.default_rng(21), steps=3, opts=opts,
                     after_step=lambda plan: rates.append(plan.balance()))
     assert bad == 0
     assert sum(1 for r in rates[-1] if r > 0) == 2
+
+
+@pytest.mark.parametrize("K", [1, 3, 16, 31])
+@pytest.mark.parametrize("vecs", [1, 2])
+@pytest.mark.parametrize("order", ["tree", "linear"])
+def test_resident_register_and_lds_tiles(fc, K, vecs, order):
+    """fp32 plans with K < 32 keep each wave's first tiles of a round in
+    registers (10 of 256 elements, or 4 of 512) and the rest in LDS: with one
+    or two blocks every round uses both; reduce, steps with raw sum and
+    broadcast, and fc_broadcast (which stages a block's range through its LDS
+    slots in pieces) against the oracle; ragged segments and tail tiles."""
+    import torch
+    rng = np.random.default_rng(K * 3 + vecs + (order == "tree"))
+    segs = table(21000 + K, "f32", nseg=7, max_len=4000) + [(0, 230_000, 1.0, 1.0), (0, 1001, 2.0, 0.0)]
+    off = 0
+    rows = []
+    for _, m, lm, dm in segs:  # re-laid end to end, 64-element aligned, so the big segment sits mid-table
+        rows.append((off, m, lm, dm))
+        off = (off + m + 63) // 64 * 64
+    for max_blocks in (1, 2):
+        opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+        p = fc.Plan(rows, K, "f32", order, **opts)
+        info = p.info()
+        per = 144 if vecs == 2 else 320
+        assert info.rounds == -(-info.ntiles // (max_blocks * per)), (info.ntiles, info.rounds)
+        p.close()
+        bad, _, _ = run_reduce(fc, rows, K, "f32", order, rng, opts=opts)
+        assert bad == 0, max_blocks
+        assert run_steps(fc, rows, K, "f32", order, rng, steps=2, opts=opts, with_out=True,
+                         with_bcast=K <= 3) == 0, max_blocks
+    n = alloc_len(rows)
+    src = host_replicas(rng, 1, n, np.float32, special=True)[0]
+    expect = oracle.broadcast(rows, src, [np.full(n, -2.0, np.float32) for _ in range(K)])
+    p = fc.Plan(rows, K, "f32", order, schedule=3, max_blocks=1, vecs_per_thread=vecs)
+    dst = torch.full((K, n), -2.0, device="cuda")
+    p.broadcast(to_dev(src), dst)
+    torch.cuda.synchronize()
+    p.close()
+    got = dst.cpu().numpy()
+    assert sum(same_bits(got[k], expect[k]) for k in range(K)) == 0
 
 
 @pytest.mark.parametrize("schedule", [2, 3])
