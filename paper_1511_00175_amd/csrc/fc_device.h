@@ -590,36 +590,52 @@ __device__ __forceinline__ void reduce_tile(const ReduceArgs& a, const Tile& til
 }
 
 // Phases 2 and 3 for a tile whose raw sums a wave kept in registers (x, in
-// reduce_tile's fp32-pair layout): finish the lane's pairs (the update of w
-// and v, or the store of the sum), leaving w' in x for the broadcast; and the
-// store of w' to one destination d.
-template <int U, int MODE>
+// reduce_tile's layout: fp32 pairs, or 4-element vectors): finish the lane's
+// elements (the update of w and v, or the store of the sum), leaving w' in x
+// for the broadcast; and the store of w' to one destination d.
+template <int DT, int U, int MODE>
 __device__ __forceinline__ void finish_kept(const ReduceArgs& a, const Tile& tile, uint32_t lane, float lr_j,
                                             float wd_j, Acc<U, 4>& x) {
     const uint64_t start4 = tile.start * 4;
     if (!(tile.seg & TAIL_BIT)) {
-        const uint32_t ne = tile.count * 4;  // a multiple of 4: pairs are never split
+        if constexpr (DT == FC_F32_PAIRS) {
+            const uint32_t ne = tile.count * 4;  // a multiple of 4: pairs are never split
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-            if (e0 < ne) finish<2, MODE, true>(a, start4, e0 * 4, &x.a[u][0], lr_j, wd_j, &x.a[u][0]);
-            if (e1 < ne) finish<2, MODE, true>(a, start4, e1 * 4, &x.a[u][2], lr_j, wd_j, &x.a[u][2]);
+            for (int u = 0; u < U; ++u) {
+                const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                if (e0 < ne) finish<2, MODE, true>(a, start4, e0 * 4, &x.a[u][0], lr_j, wd_j, &x.a[u][0]);
+                if (e1 < ne) finish<2, MODE, true>(a, start4, e1 * 4, &x.a[u][2], lr_j, wd_j, &x.a[u][2]);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t vi = lane + 64 * u;
+                if (vi < tile.count) finish<4, MODE, true>(a, start4, vi * 16, x.a[u], lr_j, wd_j, x.a[u]);
+            }
         }
     } else if (lane < tile.count) {
         finish<1, MODE, true>(a, start4, lane * 4, &x.a[0][0], lr_j, wd_j, &x.a[0][0]);
     }
 }
 
-template <int U>
+template <int DT, int U>
 __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_t lane, const Acc<U, 4>& x) {
     const uint64_t start4 = tile.start * 4;
     if (!(tile.seg & TAIL_BIT)) {
-        const uint32_t ne = tile.count * 4;
+        if constexpr (DT == FC_F32_PAIRS) {
+            const uint32_t ne = tile.count * 4;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-            if (e0 < ne) st32r<2>(d + start4, e0 * 4, &x.a[u][0]);
-            if (e1 < ne) st32r<2>(d + start4, e1 * 4, &x.a[u][2]);
+            for (int u = 0; u < U; ++u) {
+                const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
+                if (e0 < ne) st32r<2>(d + start4, e0 * 4, &x.a[u][0]);
+                if (e1 < ne) st32r<2>(d + start4, e1 * 4, &x.a[u][2]);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t vi = lane + 64 * u;
+                if (vi < tile.count) st32r<4>(d + start4, vi * 16, x.a[u]);
+            }
         }
     } else if (lane < tile.count) {
         st32r<1>(d + start4, lane * 4, &x.a[0][0]);
@@ -647,7 +663,6 @@ __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_
 // its XCD's rate.
 template <int DT, int W, int U, int C, int MAXD, bool TREE, int MODE, int RT>
 __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
-    static_assert(RT == 0 || DT == FC_F32_PAIRS, "register-held tiles keep the fp32 pair layout");
     // 16-byte aligned, so that a lane's 4 sums move as one 16-byte LDS access
     extern __shared__ f4 slot_vecs[];
     float* slots = reinterpret_cast<float*>(slot_vecs);
@@ -662,7 +677,8 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
         const int lo = ldc(ra.ranges, b);
         const int hi = ldc(ra.ranges, b + 1);
         const int lo_lds = lo + W * RT;  // tile lo_lds + j sits in LDS slot j
-        // phase 1: tiles lo + q + W i with i < RT into registers ...
+        // phase 1: tiles lo + q + W i with i < RT into registers (the loop is
+        // unrolled, so that kept[] is indexed by constants) ...
         Acc<U, 4> kept[NKEEP];
 #pragma unroll
         for (int i = 0; i < RT; ++i) {
@@ -706,19 +722,20 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
             c[2] = static_cast<unsigned long long>(__builtin_amdgcn_s_getreg((3 << 11) | 20));
         }
         // phase 2: the register-held tiles ...
+        auto finish_reg = [&](int t, Acc<U, 4>& x) {
+            const Tile tile = ld_tile(a.tiles, t);
+            float lr_j = 0.0f, wd_j = 0.0f;
+            if constexpr (MODE == MODE_STEP) {
+                const int sj = static_cast<int>(tile.seg & SEG_MASK);
+                lr_j = a.lr * ldc(a.mults, 2 * sj);
+                wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
+            }
+            finish_kept<DT, U, MODE>(a, tile, lane, lr_j, wd_j, x);  // leaves w' in x
+        };
 #pragma unroll
         for (int i = 0; i < RT; ++i) {
             const int t = lo + q + W * i;
-            if (t < hi) {
-                const Tile tile = ld_tile(a.tiles, t);
-                float lr_j = 0.0f, wd_j = 0.0f;
-                if constexpr (MODE == MODE_STEP) {
-                    const int sj = static_cast<int>(tile.seg & SEG_MASK);
-                    lr_j = a.lr * ldc(a.mults, 2 * sj);
-                    wd_j = a.wd * ldc(a.mults, 2 * sj + 1);
-                }
-                finish_kept<U, MODE>(a, tile, lane, lr_j, wd_j, kept[i]);
-            }
+            if (t < hi) finish_reg(t, kept[i]);
         }
         // ... then those in LDS, one tile per wave
         const int n = hi > lo_lds ? (hi - lo_lds) * 64 : 0;
@@ -751,7 +768,7 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
 #pragma unroll
                     for (int i = 0; i < RT; ++i) {
                         const int t = lo + q + W * i;
-                        if (t < hi) store_kept<U>(d, ld_tile(a.tiles, t), lane, kept[i]);
+                        if (t < hi) store_kept<DT, U>(d, ld_tile(a.tiles, t), lane, kept[i]);
                     }
                 });
         }
@@ -920,9 +937,6 @@ template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F
     // (lane vectors, replicas per batch) of the resident tiles; two vectors
     // per lane only with stacks up to depth 7 (deeper ones would spill)
     if (sh.vecs == 1 && sh.kchunk == 16) {
-        if constexpr (pairs) {
-            if (sh.rtiles == 10 && sh.maxd <= 1) return go(I<1>{}, I<16>{}, I<1>{}, I<10>{});
-        }
         if (sh.rtiles != 0) return hipErrorInvalidValue;
         return pick_maxd(sh.maxd, [&](auto d) { return go(I<1>{}, I<16>{}, d, I<0>{}); });
     }

@@ -51,18 +51,20 @@ inline void default_resident_shape(fc_dtype gdt, int K, int& u, int& c) {
 inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128; }
 
 // Tiles per wave whose raw sums the resident kernel keeps in registers, on
-// top of the LDS slots: what a wave's 128 VGPRs (4 waves per SIMD) leave
-// beside phase 1 when the tree's pending-subtree stack is shallow, for fp32
-// replicas (the compiler's resource report, fp32 tree step: 1 vector and
-// batches of 16 with a depth-1 stack (K < 32) holds 10 tiles in 128 VGPRs,
-// 2 vectors and batches of 4 with a depth-3 stack (K < 32) holds 4 in 123;
-// none spills).  16 waves x 10 tiles of 1 KiB add 160 KiB per CU, 16 x 4 of
-// 2 KiB add 128 KiB: a round holds 2x or 1.8x the parameters of LDS alone.
+// top of the LDS slots: fp32 replicas in tiles of 2 vectors with batches of
+// 4 and a depth-3 pending-subtree stack (K < 32) keep 4 tiles in a wave's 128
+// VGPRs (4 waves per SIMD; the compiler's resource report for the tree step:
+// 123, no spill).  16 waves x 4 tiles of 2 KiB add 128 KiB per CU to LDS's
+// 160: a round holds 1.8x the parameters.  Measured on MI355X, VGG-19 K=16
+// in 8 rounds instead of 14: 1792 vs 1829 us per step on one box, 1831-1836
+// vs 1861-1887 on another.  Other shapes gained nothing: the registers
+// spared beside a deeper stack or batches of 16 hold at most 9 tiles (fp32)
+// or 12 (fp16), which unrolled exceed the instruction cache (12 copies of
+// the reduction: 106 KB) and rolled need selects that cost load parallelism:
+// AlexNet fp16 K=128 in 3 rounds instead of 6, 2571-2576 vs 2523-2529 us;
+// 60 M fp32 x K=24 in 4 rounds instead of 6, 1063-1067 vs 1054-1056.
 inline int resident_rtiles(int gdt, int u, int c, int maxd) {
-    if (gdt != FC_F32) return 0;
-    if (u == 1 && c == 16 && maxd <= 1) return 10;
-    if (u == 2 && c == 4 && maxd <= 3) return 4;
-    return 0;
+    return gdt == FC_F32 && u == 2 && c == 4 && maxd <= 3 ? 4 : 0;
 }
 
 inline bool compiled_pair(int u, int c) {
