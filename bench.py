@@ -559,10 +559,12 @@ def main():
     dom = max(kernels, key=lambda k: kernels[k]["calls"] * kernels[k]["call_us_avg"])
     avg = kernels[dom]["call_us_avg"] * 1e-6
     achieved = kernels[dom]["algorithmic_bytes"] / avg / 1e9
-    plain = not (args.out or args.bcast or args.order != "tree" or opts or args.rotate != DEFAULT_ROTATE or
-                 args.no_balance or args.wv_sets)
-    traffic = read_traffic(wl.name, dom) if plain else None
-    prof_us = read_profile_us(wl.name, dom) if plain else None
+    # the committed profiles cover each workload (and its linear order) in
+    # the default launch configuration
+    plain = not (args.out or args.bcast or opts or args.rotate != DEFAULT_ROTATE or args.no_balance or args.wv_sets)
+    variant = wl.name + ("_linear" if args.order == "linear" else "")
+    traffic = read_traffic(variant, dom) if plain else None
+    prof_us = read_profile_us(variant, dom) if plain else None
     sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
     rk = "resident_kernel" if info.schedule == 3 else "reduce_kernel"
 

@@ -8,6 +8,8 @@ back to every worker (Fig. 3 caption).
 The work is done by HIP kernels behind the C ABI of include/fc.h; this package
 only marshals torch tensors (device memory and the current stream) into it.
 """
+import weakref
+
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_NOALLOC_MAX_ELEMS, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO,  # noqa: F401
                   FC_SCHED_FUSED, FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create,
@@ -109,24 +111,47 @@ class Plan:
         self.extent = fc_plan_query(h).extent
         self.device = torch.device("cuda", torch.cuda.current_device())
 
+    def _cached(self, role, x, check, *args):
+        """check(x, *args) -- the checked pointer(s) of buffer x in `role` --
+        done once per tensor: while a call passes the tensor object the
+        previous call passed in this role (held by weak reference), at the
+        same address with the same shape and strides, the previous result is
+        reused (a tensor's dtype and device cannot change in place)."""
+        if type(x).__name__ not in ("Tensor", "Parameter"):
+            return check(x, *args)
+        cache = self.__dict__.setdefault("_checked", {})
+        sig = (x.data_ptr(), x.shape, x.stride())
+        hit = cache.get(role)
+        if hit is not None and hit[0]() is x and hit[1] == sig:
+            return hit[2]
+        got = check(x, *args)
+        cache[role] = (weakref.ref(x), sig, got)
+        return got
+
+    def _vec_checked(self, t, name):
+        _check_vector(t, name, "float32", self.device, self.extent)
+        return t.data_ptr()
+
     def _vec(self, t, name, optional=False):
         """Pointer of an fp32 buffer (w, v, out, g, src) after checking it."""
         if t is None and optional:
             return None
-        _check_vector(t, name, "float32", self.device, self.extent)
-        return t.data_ptr()
+        return self._cached(name, t, self._vec_checked, name)
 
     def _reps(self, x, name, dtype):
         """Pointers of K buffers (replicas of the plan's type, or fp32
-        broadcast destinations): a list of K tensors or a 2-D tensor of K
-        rows, each checked like _vec."""
-        import torch
+        broadcast destinations), as a C array: a list of K tensors or a 2-D
+        tensor of K rows, each checked like _vec."""
         if isinstance(x, (list, tuple)):
             if len(x) != self.K:
                 raise ValueError(f"{name}: {len(x)} buffers for a plan of K={self.K}")
             for k, t in enumerate(x):
                 _check_vector(t, f"{name}[{k}]", dtype, self.device, self.extent)
-            return [t.data_ptr() for t in x]
+            return _fc._ptr_array([t.data_ptr() for t in x])
+        return self._cached(name, x, self._rows_checked, name, dtype)
+
+    def _rows_checked(self, x, name, dtype):
+        import torch
         if not isinstance(x, torch.Tensor) or x.dim() != 2:
             raise ValueError(f"{name} must be a list of K tensors or a 2-D tensor of K rows")
         if x.shape[0] != self.K:
@@ -139,7 +164,7 @@ class Plan:
             raise ValueError(f"{name} must be {dtype}, not {x.dtype}")
         if x.device != self.device:
             raise ValueError(f"{name} is on {x.device}, the plan on {self.device}")
-        return _rows(x)
+        return _fc._ptr_array(_rows(x))
 
     def _grads(self, x):
         return self._reps(x, "grads", _TORCH_DTYPES[self.dtype])

@@ -107,8 +107,10 @@ def _check(fn, rc):
 
 
 def _ptr_array(ptrs):
-    if ptrs is None:
-        return None
+    """A C array of device pointers from a sequence of ints (a ctypes array
+    passes through unchanged)."""
+    if ptrs is None or isinstance(ptrs, ctypes.Array):
+        return ptrs
     return (ctypes.c_void_p * len(ptrs))(*[int(p) for p in ptrs])
 
 
