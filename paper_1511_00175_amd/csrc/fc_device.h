@@ -94,6 +94,14 @@ __device__ __forceinline__ gptr_w_t gwrite(void* p) { return (gptr_w_t)p; }
 // (w' and v') ride along a 128-stream read at little cost.
 constexpr int CPOL_STREAM_LOAD = 2;   // nt
 constexpr int CPOL_RESULT_STORE = 16; // sc1
+// The resident kernel's write phases store with their own policies: the
+// update after a round's reads, which meets no read stream, with nt (measured
+// on MI355X against sc1, us per step, three alternated runs each: VGG-19
+// 1771-1774 vs 1790-1793, NiN 161.9-162.3 vs 163.8-164.2, GoogLeNet
+// 533.6-534.0 vs 536.2-537.9); the broadcast copies with sc1 (nt: GoogLeNet
+// 1180-1182 vs 1177-1180, NiN 338.4-339.4 vs 336.8-336.9).
+constexpr int CPOL_RESIDENT_STORE = 2;    // nt
+constexpr int CPOL_BROADCAST_STORE = 16;  // sc1
 
 // Raw buffer resource over [base, base + 2 GiB): word 3 = 0x00020000 is the
 // gfx9 data-format field for untyped 32-bit access.  Offsets used here are
@@ -187,22 +195,23 @@ template <> struct Rep<FC_F16, 1> {
 
 // ------------------------------------------------------------------ fp32 vectors
 // V fp32 results at byte offset `off`, stored with the result-store policy
-template <int V> __device__ __forceinline__ void st32r(gptr_w_t base, uint32_t off, const float* x) {
+template <int V, int CP = CPOL_RESULT_STORE>
+__device__ __forceinline__ void st32r(gptr_w_t base, uint32_t off, const float* x) {
     if constexpr (V == 1) {
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned int, x[0]), rsrc((const void*)base), off, 0,
-                                              CPOL_RESULT_STORE);
+                                              CP);
     } else if constexpr (V == 2) {
         f2 t;
         t.x = x[0]; t.y = x[1];
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2, t), rsrc((const void*)base), off, 0,
-                                              CPOL_RESULT_STORE);
+                                              CP);
     } else {
 #pragma unroll
         for (int q = 0; q < V / 4; ++q) {
             f4 t;
             t.x = x[4 * q + 0]; t.y = x[4 * q + 1]; t.z = x[4 * q + 2]; t.w = x[4 * q + 3];
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, t), rsrc((const void*)base), off + 16 * q, 0,
-                                                   CPOL_RESULT_STORE);
+                                                   CP);
         }
     }
 }
@@ -490,26 +499,26 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
 // reduce-only, store the sum; step, update w and v and store w', v' (and the
 // raw sum and the broadcast copies when asked for).  KEEP: instead of storing
 // the broadcast copies, leave w' in keep[0..V-1] for the caller to store.
-template <int V, int MODE, bool KEEP = false>
+template <int V, int MODE, bool KEEP = false, int CP = CPOL_RESULT_STORE>
 __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uint32_t off, const float* s,
                                        float lr_j, float wd_j, float* keep = nullptr) {
     if constexpr (MODE == MODE_REDUCE) {
-        st32r<V>(gwrite(a.out) + start4, off, s);
+        st32r<V, CP>(gwrite(a.out) + start4, off, s);
     } else {
         float w[V], v[V], wn[V], vn[V];
         ld32s<V>(gread(a.w) + start4, off, w);
         ld32s<V>(gread(a.v) + start4, off, v);
 #pragma unroll
         for (int i = 0; i < V; ++i) sgd1(s[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
-        st32r<V>(gwrite(a.w) + start4, off, wn);
-        st32r<V>(gwrite(a.v) + start4, off, vn);
-        if (a.out) st32r<V>(gwrite(a.out) + start4, off, s);
+        st32r<V, CP>(gwrite(a.w) + start4, off, wn);
+        st32r<V, CP>(gwrite(a.v) + start4, off, vn);
+        if (a.out) st32r<V, CP>(gwrite(a.out) + start4, off, s);
         if constexpr (KEEP) {
             if (a.dst)
 #pragma unroll
                 for (int i = 0; i < V; ++i) keep[i] = wn[i];
         } else if (a.dst) {
-            for (int k = 0; k < a.K; ++k) st32r<V>(gwrite(ldc(a.dst, k)) + start4, off, wn);
+            for (int k = 0; k < a.K; ++k) st32r<V, CP>(gwrite(ldc(a.dst, k)) + start4, off, wn);
         }
     }
 }
@@ -541,10 +550,10 @@ __device__ __forceinline__ void store_slots(const Tile* tiles, float* const* dst
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const uint32_t vi = lane + 64 * u;
-                    if (vi < tile.count) st32r<4>(d + start4, vi * 16, slot + vi * 4);
+                    if (vi < tile.count) st32r<4, CPOL_BROADCAST_STORE>(d + start4, vi * 16, slot + vi * 4);
                 }
             } else if (lane < tile.count) {
-                st32r<1>(d + start4, lane * 4, slot + lane);
+                st32r<1, CPOL_BROADCAST_STORE>(d + start4, lane * 4, slot + lane);
             }
         }
         __syncthreads();
@@ -603,18 +612,21 @@ __device__ __forceinline__ void finish_kept(const ReduceArgs& a, const Tile& til
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-                if (e0 < ne) finish<2, MODE, true>(a, start4, e0 * 4, &x.a[u][0], lr_j, wd_j, &x.a[u][0]);
-                if (e1 < ne) finish<2, MODE, true>(a, start4, e1 * 4, &x.a[u][2], lr_j, wd_j, &x.a[u][2]);
+                if (e0 < ne)
+                    finish<2, MODE, true, CPOL_RESIDENT_STORE>(a, start4, e0 * 4, &x.a[u][0], lr_j, wd_j, &x.a[u][0]);
+                if (e1 < ne)
+                    finish<2, MODE, true, CPOL_RESIDENT_STORE>(a, start4, e1 * 4, &x.a[u][2], lr_j, wd_j, &x.a[u][2]);
             }
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t vi = lane + 64 * u;
-                if (vi < tile.count) finish<4, MODE, true>(a, start4, vi * 16, x.a[u], lr_j, wd_j, x.a[u]);
+                if (vi < tile.count)
+                    finish<4, MODE, true, CPOL_RESIDENT_STORE>(a, start4, vi * 16, x.a[u], lr_j, wd_j, x.a[u]);
             }
         }
     } else if (lane < tile.count) {
-        finish<1, MODE, true>(a, start4, lane * 4, &x.a[0][0], lr_j, wd_j, &x.a[0][0]);
+        finish<1, MODE, true, CPOL_RESIDENT_STORE>(a, start4, lane * 4, &x.a[0][0], lr_j, wd_j, &x.a[0][0]);
     }
 }
 
@@ -627,18 +639,18 @@ __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-                if (e0 < ne) st32r<2>(d + start4, e0 * 4, &x.a[u][0]);
-                if (e1 < ne) st32r<2>(d + start4, e1 * 4, &x.a[u][2]);
+                if (e0 < ne) st32r<2, CPOL_BROADCAST_STORE>(d + start4, e0 * 4, &x.a[u][0]);
+                if (e1 < ne) st32r<2, CPOL_BROADCAST_STORE>(d + start4, e1 * 4, &x.a[u][2]);
             }
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t vi = lane + 64 * u;
-                if (vi < tile.count) st32r<4>(d + start4, vi * 16, x.a[u]);
+                if (vi < tile.count) st32r<4, CPOL_BROADCAST_STORE>(d + start4, vi * 16, x.a[u]);
             }
         }
     } else if (lane < tile.count) {
-        st32r<1>(d + start4, lane * 4, &x.a[0][0]);
+        st32r<1, CPOL_BROADCAST_STORE>(d + start4, lane * 4, &x.a[0][0]);
     }
 }
 
@@ -755,10 +767,11 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
                 for (int u = 0; u < U; ++u) {
                     const uint32_t vi = lane + 64 * u;
                     if (vi < tile.count)
-                        finish<4, MODE, true>(a, start4, vi * 16, slot + vi * 4, lr_j, wd_j, slot + vi * 4);
+                        finish<4, MODE, true, CPOL_RESIDENT_STORE>(a, start4, vi * 16, slot + vi * 4, lr_j, wd_j,
+                                                               slot + vi * 4);
                 }
             } else if (lane < tile.count) {
-                finish<1, MODE, true>(a, start4, lane * 4, slot + lane, lr_j, wd_j, slot + lane);
+                finish<1, MODE, true, CPOL_RESIDENT_STORE>(a, start4, lane * 4, slot + lane, lr_j, wd_j, slot + lane);
             }
         }
         if constexpr (MODE == MODE_STEP) {
