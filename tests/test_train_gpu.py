@@ -55,3 +55,47 @@ def test_train_rejects_a_schedule_past_its_end(fc):
         plan.train(x, w, v, dict(kind="poly", base_lr=0.1, max_iter=10), 5, 10, 0.9, 0.0, 32)
     torch.cuda.synchronize()
     assert float(w.sum()) == 128.0  # nothing was enqueued
+
+
+@pytest.mark.parametrize("schedule", [1, 3])
+def test_checkpoint_resume_is_bit_exact(fc, tmp_path, schedule):
+    """Training state is (w, v, iteration): a run stopped after iteration 17,
+    its w and v written to disk (torch.save) and loaded back into new device
+    tensors with a new plan (weights_only load), continues to the same bits as
+    an uninterrupted run, and both equal the oracle's 30 steps (the step is
+    deterministic, so resuming needs nothing else)."""
+    import torch
+    pol = POLICIES[0]
+    rng = np.random.default_rng(17 + schedule)
+    rows, ext = gen.random_table(rng, 5, 3000, 4)
+    n = (ext + 7) // 8 * 8 + 64
+    K = 12
+    reps = host_replicas(rng, K, n, np.float32, scale=0.01)
+    w = (rng.standard_normal(n) * 0.05).astype(np.float32)
+    v = np.zeros(n, np.float32)
+    ew, ev = oracle.train(rows, list(reps), w, v, 0.9, 5e-4, 256, range(30), pol)
+    r_d = to_dev(reps)
+    # uninterrupted
+    plan = fc.Plan(rows, K, "f32", "tree", schedule=schedule)
+    wa, va = to_dev(w), to_dev(v)
+    plan.train(r_d, wa, va, pol, 0, 30, 0.9, 5e-4, 256)
+    torch.cuda.synchronize()
+    plan.close()
+    # interrupted after iteration 17, state through a file
+    plan = fc.Plan(rows, K, "f32", "tree", schedule=schedule)
+    wb, vb = to_dev(w), to_dev(v)
+    plan.train(r_d, wb, vb, pol, 0, 18, 0.9, 5e-4, 256)
+    torch.cuda.synchronize()
+    plan.close()
+    path = tmp_path / "state.pt"
+    torch.save({"w": wb.cpu(), "v": vb.cpu(), "iter": 18}, path)
+    del wb, vb
+    state = torch.load(path, weights_only=True)
+    wc, vc = state["w"].cuda(), state["v"].cuda()
+    plan = fc.Plan(rows, K, "f32", "tree", schedule=schedule)
+    plan.train(r_d, wc, vc, pol, state["iter"], 30 - state["iter"], 0.9, 5e-4, 256)
+    torch.cuda.synchronize()
+    plan.close()
+    assert torch.equal(wa.view(torch.int32), wc.view(torch.int32))
+    assert torch.equal(va.view(torch.int32), vc.view(torch.int32))
+    assert same_bits(wc.cpu().numpy(), ew) == 0 and same_bits(vc.cpu().numpy(), ev) == 0
