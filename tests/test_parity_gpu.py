@@ -105,6 +105,55 @@ SHAPES = [dict(block_threads=b, vecs_per_thread=u, kchunk=c) for b in (64, 128, 
 SHAPES += [dict(schedule=2), dict(schedule=2, block_threads=256, vecs_per_thread=2, kchunk=8, max_blocks=5)]
 SHAPES += [dict(schedule=3), dict(schedule=3, max_blocks=7), dict(schedule=3, max_blocks=1)]
 
+FP16_PAIR_OPTS = [None, dict(schedule=2), dict(schedule=3), dict(schedule=3, vecs_per_thread=2, kchunk=4)]
+FP16_PAIR_OPTS += [dict(block_threads=256, vecs_per_thread=u, kchunk=c) for u, c in PAIRS]
+
+
+def fp16_pattern_replicas(K, m, pos):
+    """K fp16 replicas of m elements: every binary16 pattern in leaf pos, a
+    partner pattern (an odd multiplier makes the map a bijection of the
+    16-bit patterns) in leaf pos + 1 and +0 elsewhere; pos None: every leaf
+    holds its own bijection of the patterns."""
+    n = 1 << 16
+    bits = np.arange(n, dtype=np.uint32)
+    reps = np.zeros((K, m), np.uint16)
+    if pos is None:
+        for k in range(K):
+            reps[k, :n] = (bits * np.uint32(2 * k + 40503) + np.uint32(977 * k)) & 0xFFFF
+    else:
+        reps[pos, :n] = bits
+        reps[pos + 1, :n] = (bits * np.uint32(40503) + np.uint32(12345)) & 0xFFFF
+    return reps.view(np.float16)
+
+
+@pytest.mark.parametrize("order", ["tree", "linear"])
+@pytest.mark.parametrize("K, positions", [(16, (0, 2, 4, 6, 8, 10, 12, 14, None)), (23, (0, 6, 14, 16, 21, None))])
+def test_fp16_pair_sums_exhaustive(fc, K, positions, order):
+    """Sums of widened fp16 leaves: every binary16 pattern -- subnormals,
+    signed zeros, infinities, NaNs -- meets a partner pattern in every leaf
+    position of a chunk and of the remainder (K = 23), in both orders, for
+    every schedule and compiled fp16 shape; the raw sums and one step match
+    the oracle bit for bit."""
+    import torch
+    segs = [(0, 1 << 16, 1.0, 1.0)]
+    m = alloc_len(segs)
+    w = np.random.default_rng(K).standard_normal(m, dtype=np.float32) * np.float32(0.05)
+    for pos in positions:
+        reps = fp16_pattern_replicas(K, m, pos)
+        expect = oracle.tree_reduce(segs, list(reps), order=order, out=np.zeros(m, np.float32))
+        w1, v1, _, _ = oracle.step(segs, list(reps), w, np.zeros(m, np.float32), LR, MU, WD, 256, order=order)
+        reps_d = to_dev(reps)
+        for opts in FP16_PAIR_OPTS:
+            plan = fc.Plan(segs, K, "f16", order, **(opts or {}))
+            out = torch.zeros(m, device="cuda")
+            plan.tree_reduce(reps_d, out)
+            assert same_bits(out.cpu().numpy(), expect) == 0, (pos, opts)
+            if opts is None or "schedule" in opts:
+                w_d, v_d = to_dev(w), torch.zeros(m, device="cuda")
+                plan.step(reps_d, w_d, v_d, LR, MU, WD, 256)
+                assert same_bits(w_d.cpu().numpy(), w1) + same_bits(v_d.cpu().numpy(), v1) == 0, (pos, opts)
+            plan.close()
+
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
 def test_launch_shape_invariance(fc, dtype):
