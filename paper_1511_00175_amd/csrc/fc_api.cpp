@@ -66,6 +66,7 @@ struct fc_plan {
     hipStream_t last_stream = nullptr;  // stream of the plan's previous (uncaptured) call
     bool have_last_stream = false;
     hipEvent_t order_event = nullptr;    // orders a call on another stream after the previous one
+                                         // (created with the plan: no call creates anything)
 };
 
 namespace {
@@ -147,8 +148,6 @@ int order_after_last(fc_plan* p, hipStream_t s, bool& note) {
     // outside a capture it has since joined
     rc = capture_check(p->last_stream);
     if (rc) return rc;
-    if (!p->order_event && hipEventCreateWithFlags(&p->order_event, hipEventDisableTiming) != hipSuccess)
-        return FC_EHIP;
     if (hipEventRecord(p->order_event, p->last_stream) != hipSuccess ||
         hipStreamWaitEvent(s, p->order_event, 0) != hipSuccess)
         return FC_EHIP;
@@ -518,7 +517,8 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         fc::equal_ranges(p->ntiles, p->res_rounds, res_grid, ranges);
     }
 
-    bool ok = hipMalloc(&p->d_tiles, std::max<size_t>(tiles.size(), 1) * sizeof(Tile)) == hipSuccess &&
+    bool ok = hipEventCreateWithFlags(&p->order_event, hipEventDisableTiming) == hipSuccess &&
+              hipMalloc(&p->d_tiles, std::max<size_t>(tiles.size(), 1) * sizeof(Tile)) == hipSuccess &&
               hipMalloc(&p->d_mults, mults.size() * sizeof(float)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_grads), K * sizeof(void*)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&p->d_dst), K * sizeof(float*)) == hipSuccess;
