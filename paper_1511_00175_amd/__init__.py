@@ -32,10 +32,13 @@ def lr_at(iter, batch, **policy):
 
 def read_probe(src, out, stream=None):
     """Streaming read of the whole tensor `src` (fc_read_probe); `out` is an
-    fp32 tensor of at least fc_read_probe_blocks(src bytes) elements."""
+    fp32 tensor of at least fc_read_probe_blocks(src bytes) elements on the
+    same device."""
+    import torch
+    if not isinstance(src, torch.Tensor) or src.device.type != "cuda" or not src.is_contiguous():
+        raise ValueError("src must be a contiguous device tensor")
     nbytes = src.numel() * src.element_size()
-    if out.numel() < fc_read_probe_blocks(nbytes):
-        raise ValueError("out is too small")
+    _check_vector(out, "out", "float32", src.device, fc_read_probe_blocks(nbytes))
     rc = fc_read_probe(src.data_ptr(), nbytes, out.data_ptr(), _stream(stream))
     if rc:
         raise FcError("fc_read_probe", rc)
@@ -114,13 +117,14 @@ class Plan:
     def _cached(self, role, x, check, *args):
         """check(x, *args) -- the checked pointer(s) of buffer x in `role` --
         done once per tensor: while a call passes the tensor object the
-        previous call passed in this role (held by weak reference), at the
-        same address with the same shape and strides, the previous result is
-        reused (a tensor's dtype and device cannot change in place)."""
+        previous call passed in this role (held by weak reference), with the
+        same address, shape, strides, dtype and device (all of which `.data`
+        assignment or set_() can change in place), the previous result is
+        reused."""
         if type(x).__name__ not in ("Tensor", "Parameter"):
             return check(x, *args)
         cache = self.__dict__.setdefault("_checked", {})
-        sig = (x.data_ptr(), x.shape, x.stride())
+        sig = (x.data_ptr(), x.shape, x.stride(), x.dtype, x.get_device())
         hit = cache.get(role)
         if hit is not None and hit[0]() is x and hit[1] == sig:
             return hit[2]

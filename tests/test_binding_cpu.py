@@ -99,3 +99,33 @@ def test_other_calls_check_their_buffers(fc):
         p.train(r.half(), w, v, dict(kind="fixed", base_lr=0.1), 0, 1, 0.9, 0.0, 1)
     with pytest.raises(ValueError):
         p.step_noalloc(r, w, v[:3], 0.1, 0.9, 0.0, 1)
+
+
+def test_a_tensor_changed_in_place_is_checked_again(fc):
+    """The per-role check cache keys on the tensor's address, shape, strides,
+    dtype and device: a tensor whose storage is swapped in place (.data
+    assignment, set_) is checked again, even when its address is reused."""
+    p = fake_plan(fc)
+    r, w, v, out, dst = bufs()
+    reaches_library(fc, lambda: p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0))
+    reaches_library(fc, lambda: p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0))  # cached
+    w.data = torch.zeros(1000, dtype=torch.float64)
+    with pytest.raises(ValueError):
+        p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0)
+    w.data = torch.zeros(1000)
+    reaches_library(fc, lambda: p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0))
+    w.set_(torch.zeros(10))
+    with pytest.raises(ValueError):
+        p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0)
+    # a row tensor reshaped in place
+    w.set_(torch.zeros(1000))
+    r.set_(torch.zeros((4, 500)))
+    with pytest.raises(ValueError):
+        p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0)
+
+
+def test_read_probe_checks_its_buffers(fc):
+    with pytest.raises(ValueError):
+        fc.read_probe(torch.zeros(4096), torch.zeros(16), stream=0)  # host tensor
+    with pytest.raises(ValueError):
+        fc.read_probe(torch.zeros(8192)[::2], torch.zeros(16), stream=0)
