@@ -137,7 +137,10 @@ def fc_plan_create(segs, K, gdt=FC_F32, order=FC_ORDER_TREE, opts=None):
         rc = lib.fc_plan_create(ctypes.byref(h), arr, n, int(K), int(gdt), int(order))
     else:
         o = fc_launch_opts(0, 0, 0, 0, 0, 0)
+        fields = [f[0] for f in fc_launch_opts._fields_]
         for k, v in opts.items():
+            if k not in fields:  # a ctypes structure would keep it as a plain attribute
+                raise ValueError(f"unknown launch option {k!r} (fields: {', '.join(fields)})")
             setattr(o, k, int(v))
         rc = lib.fc_plan_create_ex(ctypes.byref(h), arr, n, int(K), int(gdt), int(order), ctypes.byref(o))
     return rc, h

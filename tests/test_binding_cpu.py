@@ -129,3 +129,8 @@ def test_read_probe_checks_its_buffers(fc):
         fc.read_probe(torch.zeros(4096), torch.zeros(16), stream=0)  # host tensor
     with pytest.raises(ValueError):
         fc.read_probe(torch.zeros(8192)[::2], torch.zeros(16), stream=0)
+
+
+def test_unknown_launch_option_is_refused(fc):
+    with pytest.raises(ValueError):
+        fc._fc.fc_plan_create([(0, 1000)], 4, opts=dict(block=64))
