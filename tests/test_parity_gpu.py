@@ -59,10 +59,11 @@ def test_step_matches_oracle(fc, K, order, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("order", ["tree", "linear"])
 @pytest.mark.parametrize("K", [1, 3, 8, 32, 100])
-def test_step_with_sum_and_broadcast(fc, K, dtype):
+def test_step_with_sum_and_broadcast(fc, K, order, dtype):
     segs = table(3000 + K, dtype, nseg=5, max_len=3000)
-    assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(K), steps=2, with_out=True,
+    assert run_steps(fc, segs, K, dtype, order, np.random.default_rng(K), steps=2, with_out=True,
                      with_bcast=True) == 0
 
 
@@ -172,15 +173,17 @@ def test_launch_shape_invariance(fc, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("order", ["tree", "linear"])
 @pytest.mark.parametrize("schedule", [1, 2, 3])
 @pytest.mark.parametrize("K", [3, 64, 130])
-def test_schedules_match_oracle(fc, K, schedule, dtype):
-    """fc_step in one fused pass and in two passes (raw sum, then update),
-    with and without the raw sum and the broadcast, over chained steps."""
+def test_schedules_match_oracle(fc, K, schedule, order, dtype):
+    """fc_step in one fused pass, in two passes (raw sum, then update) and
+    resident, with and without the raw sum and the broadcast, over chained
+    steps, in both orders."""
     segs = table(9000 + K, dtype, nseg=5, max_len=3000)
     rng = np.random.default_rng(K + schedule)
     for with_out, with_bcast in ((False, False), (True, False), (False, True), (True, True)):
-        assert run_steps(fc, segs, K, dtype, "tree", rng, steps=2, opts=dict(schedule=schedule),
+        assert run_steps(fc, segs, K, dtype, order, rng, steps=2, opts=dict(schedule=schedule),
                          with_out=with_out, with_bcast=with_bcast) == 0, (with_out, with_bcast)
 
 
