@@ -200,11 +200,13 @@ def host_info():
 
 def cpu_baseline(wl, reps_h, w_h, v_h, order, target_s=10.0):
     """Time the oracle on a contiguous window [0, m) of the workload's
-    elements, all K replicas, from host copies of the inputs: once on one
-    host core (oracle.step; the window grown to about target_s seconds, or
-    the whole step), then on every host thread (oracle.step_parallel: one
-    range of elements per thread, the same arithmetic for every element),
-    best of 3.  Returns the JSON object."""
+    elements, all K replicas, from host copies of the inputs: on one host
+    core (oracle.step; the window grown to about target_s seconds, or the
+    whole step, repeated until about target_s seconds of work), then on every
+    host thread (oracle.step_parallel: one range of elements per thread, the
+    same arithmetic for every element; at least 3 runs, repeated until the
+    threads have done about target_s seconds of work).  Each leg reports its
+    fastest run.  Returns the JSON object."""
     import oracle
 
     table = wl.table()
@@ -219,6 +221,13 @@ def cpu_baseline(wl, reps_h, w_h, v_h, order, target_s=10.0):
         oracle.step(rows, list(reps_h[:, :m]), w_h[:m], v_h[:m], wl.lr, wl.mu, wl.wd, wl.batch, order=order)
         return time.perf_counter() - t0, sum(n for _, n, _, _ in rows)
 
+    def repeat(fn, threads, min_runs, times):
+        # fastest of at least min_runs runs, and of as many as make about
+        # target_s seconds of work over `threads` threads
+        while len(times) < min_runs or (sum(times) * threads < target_s and len(times) < 1000):
+            times.append(fn())
+        return min(times), len(times), sum(times)
+
     total = max(o + n for o, n, _, _ in table)
     m = min(total, 1 << 16)
     dt, n = run(m)
@@ -227,22 +236,27 @@ def cpu_baseline(wl, reps_h, w_h, v_h, order, target_s=10.0):
     if m2 > m:
         dt, n = run(m2)
         m = m2
+    dt, runs1, _ = repeat(lambda: run(m)[0], 1, 1, [dt])
     bytes_ = n * (wl.K * wl.s_g + 16)
     model, ncpu = host_info()
     nthreads = oracle.default_threads()
     rows = window(m)
-    dt_mt = float("inf")
-    for _ in range(3):
+
+    def run_mt():
         t0 = time.perf_counter()
         oracle.step_parallel(rows, reps_h[:, :m], w_h[:m], v_h[:m], wl.lr, wl.mu, wl.wd, wl.batch, order=order,
                              threads=nthreads)
-        dt_mt = min(dt_mt, time.perf_counter() - t0)
+        return time.perf_counter() - t0
+
+    dt_mt, runs_mt, wall_mt = repeat(run_mt, nthreads, 3, [])
     return {"value": round(bytes_ / dt_mt / 1e9, 4), "unit": "GB/s", "cores": nthreads, "kind": "oracle",
             "sample": f"{n} of {wl.n_params} parameters (elements [0, {m}) of the layout), all K={wl.K} "
                       f"replicas, one fused step, cut into {nthreads} element ranges run on {nthreads} host "
-                      f"threads (best of 3: {dt_mt:.3f} s) of {ncpu} ({model})",
-            "seconds": round(dt_mt, 3), "us_per_step_equiv": round(dt_mt / n * wl.n_params * 1e6, 1),
-            "single_thread": {"value": round(bytes_ / dt / 1e9, 4), "seconds": round(dt, 3), "cores": 1}}
+                      f"threads (fastest of {runs_mt} runs, {wall_mt:.2f} s in all: {dt_mt:.3f} s) of {ncpu} "
+                      f"({model})",
+            "seconds": round(dt_mt, 3), "runs": runs_mt, "us_per_step_equiv": round(dt_mt / n * wl.n_params * 1e6, 1),
+            "single_thread": {"value": round(bytes_ / dt / 1e9, 4), "seconds": round(dt, 3), "cores": 1,
+                              "runs": runs1}}
 
 
 FIG4_KS = (1, 2, 4, 8, 16, 32, 64, 128)
