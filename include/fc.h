@@ -108,9 +108,10 @@ typedef struct fc_plan fc_plan;
  *   pure read stream) and then updates them from there, so the raw sum never
  *   goes to HBM.  A block's share per round is what one compute unit holds:
  *   its LDS (1 KiB per 256-element tile: about 10 M parameters per round over
- *   256 compute units of 160 KiB), plus, for fp32 replicas in tiles of 2
- *   vectors with K < 32, the tiles its waves keep in registers (0.8x as much
- *   again); larger plans take several rounds, one launch per round.  It
+ *   256 compute units of 160 KiB), plus, when that saves rounds, the tiles
+ *   its waves keep in registers (fp32 replicas in tiles of 2 vectors with
+ *   K < 32: 0.8x as much again; fp16 replicas with K < 512: 0.4x); larger
+ *   plans take several rounds, one launch per round.  It
  *   also makes fc_tree_reduce store the sums only after each read phase.
  *   Tiles of 64 lanes x 1 vector with batches of 16 replicas (default), or x 2
  *   vectors with batches of 4 (vecs_per_thread 2, K < 512).

@@ -403,15 +403,22 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         res_tiles += (segs[j].length / vec + tile_vecs_r - 1) / tile_vecs_r + (segs[j].length % vec ? 1 : 0);
     const uint64_t slot_bytes = fc::RESIDENT_SLOT * sizeof(float) * res_u;
     const uint64_t cap_lds = std::max<uint64_t>(1, static_cast<uint64_t>(std::max(lds_cu, 0)) / slot_bytes);
-    // a block's tiles in one round: the waves' register-held tiles first,
-    // then LDS slots
-    const int res_rt = fc::resident_rtiles(gdt, res_u, res_c, bit_length(K / res_c));
-    const uint64_t in_regs = static_cast<uint64_t>(fc::RESIDENT_WAVES) * res_rt;
-    const uint64_t cap = cap_lds + in_regs;
     int res_grid = std::max(1, cus);
     if (opts && opts->max_blocks > 0) res_grid = std::min(res_grid, opts->max_blocks);
     if (res_tiles > 0 && res_tiles < static_cast<uint64_t>(res_grid)) res_grid = static_cast<int>(res_tiles);
-    const uint64_t res_rounds = std::max<uint64_t>(1, (res_tiles + res_grid * cap - 1) / (res_grid * cap));
+    auto rounds_for = [&](uint64_t per_block) {
+        const uint64_t per_round = static_cast<uint64_t>(res_grid) * per_block;
+        return std::max<uint64_t>(1, (res_tiles + per_round - 1) / per_round);
+    };
+    // a block's tiles in one round: the waves' register-held tiles first,
+    // then LDS slots; the register-held tiles are used only when they save
+    // rounds (their kernel instance is larger)
+    int res_rt = fc::resident_rtiles(gdt, res_u, res_c, bit_length(K / res_c));
+    if (res_rt > 0 && rounds_for(cap_lds + static_cast<uint64_t>(fc::RESIDENT_WAVES) * res_rt) >= rounds_for(cap_lds))
+        res_rt = 0;
+    const uint64_t in_regs = static_cast<uint64_t>(fc::RESIDENT_WAVES) * res_rt;
+    const uint64_t cap = cap_lds + in_regs;
+    const uint64_t res_rounds = rounds_for(cap);
     const uint64_t res_ranges = static_cast<uint64_t>(res_grid) * res_rounds;
     // LDS for the most tiles a block may ever hold beyond its registers, so
     // that rebalanced ranges (fc_plan_balance) never need more than a launch

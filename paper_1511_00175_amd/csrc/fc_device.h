@@ -950,6 +950,9 @@ template <int DT, class F> hipError_t pick_resident(const Shape& sh, int mode, F
     // (lane vectors, replicas per batch) of the resident tiles; two vectors
     // per lane only with stacks up to depth 7 (deeper ones would spill)
     if (sh.vecs == 1 && sh.kchunk == 16) {
+        if constexpr (DT == FC_F16) {
+            if (sh.rtiles == 4 && sh.maxd <= 5) return go(I<1>{}, I<16>{}, I<5>{}, I<4>{});
+        }
         if (sh.rtiles != 0) return hipErrorInvalidValue;
         return pick_maxd(sh.maxd, [&](auto d) { return go(I<1>{}, I<16>{}, d, I<0>{}); });
     }

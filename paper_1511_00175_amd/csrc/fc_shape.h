@@ -51,19 +51,24 @@ inline void default_resident_shape(fc_dtype gdt, int K, int& u, int& c) {
 inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128; }
 
 // Tiles per wave whose raw sums the resident kernel keeps in registers, on
-// top of the LDS slots: fp32 replicas in tiles of 2 vectors with batches of
-// 4 and a depth-3 pending-subtree stack (K < 32) keep 4 tiles in a wave's 128
-// VGPRs (4 waves per SIMD; the compiler's resource report for the tree step:
-// 123, no spill).  16 waves x 4 tiles of 2 KiB add 128 KiB per CU to LDS's
-// 160: a round holds 1.8x the parameters.  Measured on MI355X, VGG-19 K=16
-// in 8 rounds instead of 14: 1792 vs 1829 us per step on one box, 1831-1836
-// vs 1861-1887 on another.  Other shapes gained nothing: the registers
-// spared beside a deeper stack or batches of 16 hold at most 9 tiles (fp32)
-// or 12 (fp16), which unrolled exceed the instruction cache (12 copies of
-// the reduction: 106 KB) and rolled need selects that cost load parallelism:
-// AlexNet fp16 K=128 in 3 rounds instead of 6, 2571-2576 vs 2523-2529 us;
-// 60 M fp32 x K=24 in 4 rounds instead of 6, 1063-1067 vs 1054-1056.
+// top of the LDS slots (the plan uses them only when they save rounds: the
+// kernel instance that holds them is about 4x larger).  16 waves x 4 tiles
+// per CU: fp32 replicas in tiles of 2 vectors (2 KiB of sums each) with
+// batches of 4 and a depth-3 pending-subtree stack (K < 32; 123 VGPRs for
+// the tree step, no spill), 1.8x the parameters of LDS alone per round;
+// fp16 replicas in tiles of 1 vector (1 KiB) with batches of 16 and a stack
+// of depth 5 (K < 512; 92 VGPRs), 1.4x.  Measured on MI355X (us per step):
+// VGG-19 K=16 in 8 rounds instead of 14, 1792 vs 1829 on one box, 1831-1836
+// vs 1861-1887 on another; AlexNet fp16 K=128 in 5 rounds instead of 6,
+// 2466.9 vs 2500.2 (both builds alternated in one process; 2469 vs 2496 in
+// the parameter-server order).  Not kept: 6 fp16 tiles (4 rounds) 2511.3
+// vs 2468.9 with 4 -- the kernel outgrows the instruction cache, as 12
+// unrolled tiles (106 KB) and rolled ones (selects that cost load
+// parallelism: AlexNet fp16 in 3 rounds 2571-2576 vs 2523-2529) did; fp32
+// tiles of 1 vector with K < 512, 4 per wave: VGG-19-sized K=32 in 10
+// rounds instead of 14, 3098.0 vs 3117.4, 60 M x K=32 1297.5 vs 1297.7.
 inline int resident_rtiles(int gdt, int u, int c, int maxd) {
+    if (gdt == FC_F16 && u == 1 && c == 16 && maxd <= 5) return 4;
     return gdt == FC_F32 && u == 2 && c == 4 && maxd <= 3 ? 4 : 0;
 }
 

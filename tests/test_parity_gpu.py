@@ -215,10 +215,10 @@ def test_schedule_resolution(fc):
         if dtype == "f32" and K <= 16:
             # tiles of 2 vectors per lane, batches of 4: 2 tiles of 512 elements
             # (the second of 488), then the 5-element segment's vector and its
-            # tail tile; the 4 tiles a block could be given fit its waves'
-            # registers (4 tiles each), so LDS keeps its one-slot minimum, 2 KiB
+            # tail tile; one round either way, so no register-held tiles: LDS
+            # for the 4 tiles a block could be given, 2 KiB each
             assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 2, 4, 1)
-            assert (info.ntiles, info.grid, info.lds_bytes) == (4, 4, 2048)
+            assert (info.ntiles, info.grid, info.lds_bytes) == (4, 4, 4 * 2048)
         else:
             assert (info.block_threads, info.vecs_per_thread, info.kchunk, info.k_waves) == (1024, 1, 16, 1)
             # 3 tiles of 256 elements and one of 232, then the 5-element segment's
@@ -534,8 +534,9 @@ def test_resident_plans_with_different_lds_interleave(fc):
     rng = np.random.default_rng(77)
     big = fc.Plan(rows_big, K, "f32", "tree", schedule=3)
     small = fc.Plan(rows_small, K, "f32", "tree", schedule=3)
-    # 6 tiles of 512 fit the small plan's registers: one LDS slot
-    assert big.info().lds_bytes == 160 * 1024 and small.info().lds_bytes == 2 * 1024
+    # the small plan's 6 tiles of 512 take one round with or without
+    # register-held tiles, so they sit in 6 LDS slots of 2 KiB
+    assert big.info().lds_bytes == 160 * 1024 and small.info().lds_bytes == 6 * 2 * 1024
     reps = torch.from_numpy(rng.standard_normal((K, big_n), dtype=np.float32)).cuda()
     out = torch.full((big_n,), -1.0, device="cuda")
     big.tree_reduce(reps, out)
@@ -561,30 +562,36 @@ def test_batch_not_a_power_of_two(fc, batch):
                          batch=batch) == 0, schedule
 
 
-@pytest.mark.parametrize("n,K,max_blocks,vecs", [(1000, 4, 0, 1), (5_000_000, 8, 0, 1), (40_000_000, 8, 0, 1),
-                                                 (143_667_240, 16, 0, 1), (143_667_240, 16, 0, 2),
-                                                 (60_965_224, 128, 0, 2), (60_965_224, 32, 0, 1),
-                                                 (300_000, 8, 3, 1), (300_000, 8, 3, 2), (1, 1, 0, 1)])
-def test_resident_partition(fc, n, K, max_blocks, vecs):
+@pytest.mark.parametrize("n,K,max_blocks,vecs,dtype", [
+    (1000, 4, 0, 1, "f32"), (5_000_000, 8, 0, 1, "f32"), (40_000_000, 8, 0, 1, "f32"),
+    (143_667_240, 16, 0, 1, "f32"), (143_667_240, 16, 0, 2, "f32"), (60_965_224, 128, 0, 2, "f32"),
+    (60_965_224, 32, 0, 1, "f32"), (300_000, 8, 3, 1, "f32"), (300_000, 8, 3, 2, "f32"), (1, 1, 0, 1, "f32"),
+    (60_965_224, 128, 0, 1, "f16"), (60_965_224, 600, 0, 1, "f16"), (5_000_000, 64, 0, 1, "f16"),
+    (300_000, 16, 3, 1, "f16"), (1000, 4, 0, 1, "f16")])
+def test_resident_partition(fc, n, K, max_blocks, vecs, dtype):
     """The resident plan's grid, rounds and LDS per block follow from the tile
     count, the CU's LDS and the tiles its waves hold in registers: rounds =
     ceil(tiles / (grid * (slots + 16 * rt))) for tiles of 64 * vecs vectors,
-    each with 1 KiB * vecs of LDS (160 KiB per CU), rt = 4 register-held
-    tiles per wave for 2 vectors with K < 32, else 0; a
-    block's LDS holds the slots of as many tiles as it could be given in one
-    round beyond its registers (a round's tiles, at most the CU's capacity),
-    so that rebalanced ranges never need more."""
+    each with 1 KiB * vecs of LDS (160 KiB per CU); rt = 4 register-held
+    tiles per wave for fp32 tiles of 2 vectors with K < 32 and fp16 tiles of
+    1 vector with K < 512 when they save rounds, else 0; a block's LDS holds
+    the slots of as many tiles as it could be given in one round beyond its
+    registers (a round's tiles, at most the CU's capacity), so that
+    rebalanced ranges never need more."""
     import math
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    p = fc.Plan([(0, n, 1, 1)], K, "f32", "tree", schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    p = fc.Plan([(0, n, 1, 1)], K, dtype, "tree", schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
     info = p.info()
     p.close()
     tiles = (n // 4 + 64 * vecs - 1) // (64 * vecs) + (1 if n % 4 else 0)
     grid = min(cus, max_blocks) if max_blocks else cus
     grid = min(grid, tiles)
     slots = (160 * 1024) // (1024 * vecs)
-    regs = 16 * (4 if vecs == 2 and K < 32 else 0)
+    rt = (dtype == "f32" and vecs == 2 and K < 32) or (dtype == "f16" and vecs == 1 and K < 512)
+    regs = 16 * 4 if rt else 0
+    if regs and math.ceil(tiles / (grid * (slots + regs))) >= math.ceil(tiles / (grid * slots)):
+        regs = 0
     rounds = max(1, math.ceil(tiles / (grid * (slots + regs))))
     per = max(1, min(slots + regs, max(1, math.ceil(tiles / rounds))) - regs)
     assert (info.ntiles, info.grid, info.rounds, info.lds_bytes) == (tiles, grid, rounds, per * 1024 * vecs), \
@@ -900,40 +907,45 @@ def test_balance_drains_the_plans_stream(fc):
     p.close()
 
 
-@pytest.mark.parametrize("K,vecs,per_block", [(40, 1, 160), (6, 2, 144)])
-def test_balance_with_full_lds_keeps_equal_shares(fc, K, vecs, per_block):
+@pytest.mark.parametrize("K,vecs,per_block,dtype", [(40, 1, 160, "f32"), (6, 2, 144, "f32"), (40, 1, 224, "f16")])
+def test_balance_with_full_lds_keeps_equal_shares(fc, K, vecs, per_block, dtype):
     """Two blocks whose equal share of each round already fills the block
-    (2 rounds: 160 LDS slots of 256-element tiles; or, with 2 vectors, 80
-    slots and 64 tiles in its waves' registers, of 512 elements): no unequal
+    (2 rounds: 160 LDS slots of 256-element tiles; with fp32 tiles of 2
+    vectors, 80 slots and 64 tiles of 512 elements in its waves' registers;
+    with fp16 replicas, 160 slots and 64 tiles in registers): no unequal
     division fits, so the shares fc_plan_balance writes stay equal; the steps
     after it stay bit-exact."""
     n = 2 * 2 * per_block * 256 * vecs
     segs = [(0, n, 1.0, 1.0)]
     opts = dict(schedule=3, max_blocks=2, vecs_per_thread=vecs)
-    p = fc.Plan(segs, K, "f32", "tree", **opts)
+    p = fc.Plan(segs, K, dtype, "tree", **opts)
     info = p.info()
     p.close()
     assert (info.ntiles, info.rounds, info.lds_bytes) == (4 * per_block, 2, 160 * 1024)
     rates = []
-    bad = run_steps(fc, segs, K, "f32", "tree", np.random.default_rng(21), steps=3, opts=opts,
+    bad = run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(21), steps=3, opts=opts,
                     after_step=lambda plan: rates.append(plan.balance()))
     assert bad == 0
     assert sum(1 for r in rates[-1] if r > 0) == 2
 
 
 @pytest.mark.parametrize("K,dtype,vecs", [(1, "f32", 2), (3, "f32", 2), (16, "f32", 2), (31, "f32", 2),
-                                          (16, "f32", 1), (128, "f16", 1)])
+                                          (16, "f32", 1), (16, "f16", 1), (128, "f16", 1), (300, "f16", 1),
+                                          (600, "f16", 1)])
 @pytest.mark.parametrize("order", ["tree", "linear"])
 def test_resident_register_and_lds_tiles(fc, K, dtype, vecs, order):
-    """fp32 plans with tiles of 2 vectors and K < 32 keep each wave's first 4
-    tiles (of 512 elements) of a round in registers and the rest in LDS: with
-    one or two blocks every round uses both (the other shapes, LDS only, over
-    many rounds); reduce, steps with raw sum and broadcast, and fc_broadcast
-    (which stages a block's range through its LDS slots in pieces) against
-    the oracle; ragged segments and tail tiles."""
+    """fp32 plans with tiles of 2 vectors (512 elements) and K < 32, and fp16
+    plans (tiles of 256 elements) with K < 512, keep each wave's first 4
+    tiles of a round in registers and the rest in LDS when that saves
+    rounds: here with one block, and with two for most cases, every round
+    uses both (the other shapes, LDS only, over many rounds); reduce, steps
+    with raw sum and broadcast, and fc_broadcast (which stages a block's
+    range through its LDS slots in pieces) against the oracle; ragged
+    segments and tail tiles."""
+    import math
     import torch
     rng = np.random.default_rng(K * 3 + vecs + (order == "tree") + (dtype == "f16") * 7)
-    big = 230_000 if K < 200 else 120_000
+    big = (300_000 if dtype == "f16" else 230_000) if K < 200 else 120_000
     segs = table(21000 + K, dtype, nseg=7, max_len=4000) + [(0, big, 1.0, 1.0), (0, 1001, 2.0, 0.0)]
     off = 0
     rows = []
@@ -944,9 +956,14 @@ def test_resident_register_and_lds_tiles(fc, K, dtype, vecs, order):
         opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
         p = fc.Plan(rows, K, dtype, order, **opts)
         info = p.info()
-        per = 144 if vecs == 2 else 160
-        assert info.rounds == -(-info.ntiles // (max_blocks * per)) >= 1, (info.ntiles, info.rounds)
-        assert info.ntiles > max_blocks * (64 if vecs == 2 else 0), info.ntiles
+        slots = 160 // vecs
+        rt = (dtype == "f32" and vecs == 2 and K < 32) or (dtype == "f16" and K < 512)
+        lds_rounds = math.ceil(info.ntiles / (max_blocks * slots))
+        rt_rounds = math.ceil(info.ntiles / (max_blocks * (slots + 64)))
+        used = rt and rt_rounds < lds_rounds
+        assert info.rounds == (rt_rounds if used else lds_rounds) >= 1, (info.ntiles, info.rounds)
+        assert used or not rt or max_blocks == 2, (info.ntiles, info.rounds)
+        assert info.ntiles > max_blocks * (64 if used else 0), info.ntiles
         p.close()
         bad, _, _ = run_reduce(fc, rows, K, dtype, order, rng, opts=opts)
         assert bad == 0, max_blocks
