@@ -61,12 +61,14 @@ inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128;
 // VGG-19 K=16 in 8 rounds instead of 14, 1792 vs 1829 on one box, 1831-1836
 // vs 1861-1887 on another; AlexNet fp16 K=128 in 5 rounds instead of 6,
 // 2466.9 vs 2500.2 (both builds alternated in one process; 2469 vs 2496 in
-// the parameter-server order).  Not kept: 6 fp16 tiles (4 rounds) 2511.3
-// vs 2468.9 with 4 -- the kernel outgrows the instruction cache, as 12
-// unrolled tiles (106 KB) and rolled ones (selects that cost load
-// parallelism: AlexNet fp16 in 3 rounds 2571-2576 vs 2523-2529) did; fp32
-// tiles of 1 vector with K < 512, 4 per wave: VGG-19-sized K=32 in 10
-// rounds instead of 14, 3098.0 vs 3117.4, 60 M x K=32 1297.5 vs 1297.7.
+// the parameter-server order).  Not kept: 5 or 6 fp16 tiles, which give
+// AlexNet 4 rounds, 2497.8 and 2511.3 vs 2469.3 and 2468.9 with 4 tiles
+// (4 rounds are slower whichever way they are reached; the instance with 5
+// is smaller than the one with 6, so code size is not the cause); 12
+// unrolled tiles (106 KB of code) and rolled ones (selects that cost load
+// parallelism: AlexNet fp16 in 3 rounds 2571-2576 vs 2523-2529); fp32 tiles
+// of 1 vector with K < 512, 4 per wave: VGG-19-sized K=32 in 10 rounds
+// instead of 14, 3098.0 vs 3117.4, 60 M x K=32 1297.5 vs 1297.7.
 inline int resident_rtiles(int gdt, int u, int c, int maxd) {
     if (gdt == FC_F16 && u == 1 && c == 16 && maxd <= 5) return 4;
     return gdt == FC_F32 && u == 2 && c == 4 && maxd <= 3 ? 4 : 0;
