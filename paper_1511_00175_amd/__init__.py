@@ -73,6 +73,15 @@ def _rows(x):
 _TORCH_DTYPES = {"f32": "float32", "f16": "float16"}
 
 
+_STEP_CACHE = 64  # sets of step buffers whose checks are kept per plan
+
+
+def _sig(x):
+    """What a tensor's checks depend on and `.data` assignment or set_() can
+    change in place: address, shape, strides, dtype, device."""
+    return (x.data_ptr(), x.shape, x.stride(), x.dtype, x.get_device())
+
+
 def _check_vector(t, name, dtype, device, n):
     """`t` must be a contiguous torch tensor of `dtype` on `device` holding at
     least n elements (the C ABI sees only the pointer, so a short or
@@ -101,6 +110,8 @@ class Plan:
               2 two-pass, 3 resident); results do not depend on them.
     """
 
+    _step_cache = None  # {buffer ids: (weak references, signatures, checked pointers)}
+
     def __init__(self, segments, K, dtype="f32", order="tree", **opts):
         import torch
         rc, h = fc_plan_create(segments, K, _DTYPES[dtype], _ORDERS[order], opts or None)
@@ -124,7 +135,7 @@ class Plan:
         if type(x).__name__ not in ("Tensor", "Parameter"):
             return check(x, *args)
         cache = self.__dict__.setdefault("_checked", {})
-        sig = (x.data_ptr(), x.shape, x.stride(), x.dtype, x.get_device())
+        sig = _sig(x)
         hit = cache.get(role)
         if hit is not None and hit[0]() is x and hit[1] == sig:
             return hit[2]
@@ -230,8 +241,33 @@ class Plan:
             raise FcError("fc_train", rc)
 
     def _step_args(self, grads, w, v, out, bcast):
-        return (self._grads(grads), self._vec(w, "w"), self._vec(v, "v"), self._vec(out, "out", optional=True),
-                None if bcast is None else self._reps(bcast, "bcast", "float32"))
+        """Checked pointers of a step's buffers.  The results of the last
+        _STEP_CACHE distinct sets of tensors are kept (by weak reference, with
+        each tensor's address, shape, strides, dtype and device), so that
+        steps that cycle through a few sets of buffers -- double-buffered
+        gradients, rotating weights -- are checked once per set; any other
+        call checks every buffer (_vec, _reps)."""
+        key = (id(grads), id(w), id(v), id(out), id(bcast))
+        cache = self._step_cache
+        hit = cache.get(key) if cache is not None else None
+        if hit is not None:
+            refs, sigs, got = hit
+            if (refs[0]() is grads and refs[1]() is w and refs[2]() is v
+                    and (out is None if refs[3] is None else refs[3]() is out)
+                    and (bcast is None if refs[4] is None else refs[4]() is bcast)
+                    and sigs == (_sig(grads), _sig(w), _sig(v), out is not None and _sig(out),
+                                 bcast is not None and _sig(bcast))):
+                return got
+        got = (self._grads(grads), self._vec(w, "w"), self._vec(v, "v"), self._vec(out, "out", optional=True),
+               None if bcast is None else self._reps(bcast, "bcast", "float32"))
+        bufs = (grads, w, v, out, bcast)
+        if all(b is None or type(b).__name__ in ("Tensor", "Parameter") for b in bufs) and grads is not None:
+            if cache is None or len(cache) >= _STEP_CACHE:
+                cache = self._step_cache = {}
+            cache[key] = (tuple(None if b is None else weakref.ref(b) for b in bufs),
+                          (_sig(grads), _sig(w), _sig(v), out is not None and _sig(out),
+                           bcast is not None and _sig(bcast)), got)
+        return got
 
     def step(self, grads, w, v, lr, mu, wd, batch, out=None, bcast=None, stream=None):
         g, wp, vp, op, bp = self._step_args(grads, w, v, out, bcast)

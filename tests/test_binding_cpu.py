@@ -134,3 +134,22 @@ def test_read_probe_checks_its_buffers(fc):
 def test_unknown_launch_option_is_refused(fc):
     with pytest.raises(ValueError):
         fc._fc.fc_plan_create([(0, 1000)], 4, opts=dict(block=64))
+
+
+def test_rotating_buffers_are_each_checked(fc):
+    """Steps that cycle through several sets of buffers reuse each set's
+    checks; a tensor created after another was freed (and that may take its
+    id) is checked on its own."""
+    import gc
+    p = fake_plan(fc)
+    sets = [bufs()[:3] for _ in range(3)]
+    for _ in range(2):
+        for r, w, v in sets:
+            reaches_library(fc, lambda: p.step(r, w, v, 0.1, 0.9, 0.0, 1, stream=0))
+    r, w, v = sets[1]
+    del sets, w
+    gc.collect()
+    for _ in range(50):  # new tensors, some of which reuse freed ids
+        short = torch.zeros(999)
+        with pytest.raises(ValueError):
+            p.step(r, short, v, 0.1, 0.9, 0.0, 1, stream=0)
