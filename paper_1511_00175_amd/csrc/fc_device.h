@@ -497,8 +497,13 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
 
 // The end of the work on one lane-vector whose raw sum s[0..V-1] is known:
 // reduce-only, store the sum; step, update w and v and store w', v' (and the
-// raw sum and the broadcast copies when asked for).  KEEP: instead of storing
-// the broadcast copies, leave w' in keep[0..V-1] for the caller to store.
+// raw sum and the broadcast copies when asked for).  KEEP (the resident
+// kernel): with a broadcast, leave w' in keep[0..V-1] instead of storing the
+// copies; without one, store w' and leave v' in keep[0..V-1] instead of
+// storing it, for the caller to store after the block's w' stores (measured
+// on MI355X with both builds alternated in one process, us per step: VGG-19
+// K=16 1763.3 vs 1775.5, GoogLeNet 536.5 vs 537.7, NiN and AlexNet fp16
+// unchanged).  The caller's keep may alias s.
 template <int V, int MODE, bool KEEP = false, int CP = CPOL_RESULT_STORE>
 __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uint32_t off, const float* s,
                                        float lr_j, float wd_j, float* keep = nullptr) {
@@ -511,12 +516,16 @@ __device__ __forceinline__ void finish(const ReduceArgs& a, uint64_t start4, uin
 #pragma unroll
         for (int i = 0; i < V; ++i) sgd1(s[i], w[i], v[i], lr_j, a.mu, wd_j, a.c, wn[i], vn[i]);
         st32r<V, CP>(gwrite(a.w) + start4, off, wn);
-        st32r<V, CP>(gwrite(a.v) + start4, off, vn);
+        if (!KEEP || a.dst) st32r<V, CP>(gwrite(a.v) + start4, off, vn);
         if (a.out) st32r<V, CP>(gwrite(a.out) + start4, off, s);
         if constexpr (KEEP) {
-            if (a.dst)
+            if (a.dst) {
 #pragma unroll
                 for (int i = 0; i < V; ++i) keep[i] = wn[i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < V; ++i) keep[i] = vn[i];
+            }
         } else if (a.dst) {
             for (int k = 0; k < a.K; ++k) st32r<V, CP>(gwrite(ldc(a.dst, k)) + start4, off, wn);
         }
@@ -630,7 +639,7 @@ __device__ __forceinline__ void finish_kept(const ReduceArgs& a, const Tile& til
     }
 }
 
-template <int DT, int U>
+template <int DT, int U, int CP = CPOL_BROADCAST_STORE>
 __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_t lane, const Acc<U, 4>& x) {
     const uint64_t start4 = tile.start * 4;
     if (!(tile.seg & TAIL_BIT)) {
@@ -639,18 +648,18 @@ __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t e0 = 256 * u + 2 * lane, e1 = e0 + 128;
-                if (e0 < ne) st32r<2, CPOL_BROADCAST_STORE>(d + start4, e0 * 4, &x.a[u][0]);
-                if (e1 < ne) st32r<2, CPOL_BROADCAST_STORE>(d + start4, e1 * 4, &x.a[u][2]);
+                if (e0 < ne) st32r<2, CP>(d + start4, e0 * 4, &x.a[u][0]);
+                if (e1 < ne) st32r<2, CP>(d + start4, e1 * 4, &x.a[u][2]);
             }
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t vi = lane + 64 * u;
-                if (vi < tile.count) st32r<4, CPOL_BROADCAST_STORE>(d + start4, vi * 16, x.a[u]);
+                if (vi < tile.count) st32r<4, CP>(d + start4, vi * 16, x.a[u]);
             }
         }
     } else if (lane < tile.count) {
-        st32r<1, CPOL_BROADCAST_STORE>(d + start4, lane * 4, &x.a[0][0]);
+        st32r<1, CP>(d + start4, lane * 4, &x.a[0][0]);
     }
 }
 
@@ -662,8 +671,11 @@ __device__ __forceinline__ void store_kept(gptr_w_t d, const Tile& tile, uint32_
 // first RT tiles in registers, the others in the tile's LDS slot in element
 // order; HBM sees a pure read stream, no writes.  Phase 2, after a barrier:
 // wave q finishes the same tiles (the SGD update, or the store of the raw
-// sum), from its registers and from LDS; with a broadcast, phase 3 stores w'
-// to the K copies one destination at a time (store_slots).  The registers
+// sum), from its registers and from LDS; a step without a broadcast stores
+// w' there and parks v' where the sums were, and after another barrier
+// stores v' as a pure write stream; with a broadcast, phase 2 stores w' and
+// v' and phase 3 stores w' to the K copies one destination at a time
+// (store_slots).  The registers
 // multiply what one round holds: LDS holds 160 KiB per CU, and RT tiles of
 // 64 lanes x U vectors per wave add 16 * RT * U KiB.  In round r the blocks'
 // ranges are neighbours, so the whole grid streams one region of the
@@ -772,6 +784,33 @@ __global__ __launch_bounds__(64 * W) void resident_kernel(ResidentArgs ra) {
                 }
             } else if (lane < tile.count) {
                 finish<1, MODE, true, CPOL_RESIDENT_STORE>(a, start4, lane * 4, slot + lane, lr_j, wd_j, slot + lane);
+            }
+        }
+        if constexpr (MODE == MODE_STEP) {
+            if (!a.dst) {
+                // phase 2b: v', parked in the registers and slots by phase 2,
+                // stored after the block's w' stores as a pure write stream
+                __syncthreads();
+#pragma unroll
+                for (int i = 0; i < RT; ++i) {
+                    const int t = lo + q + W * i;
+                    if (t < hi) store_kept<DT, U, CPOL_RESIDENT_STORE>(gwrite(a.v), ld_tile(a.tiles, t), lane, kept[i]);
+                }
+                for (int j = q; j < hi - lo_lds; j += W) {
+                    const Tile tile = ld_tile(a.tiles, lo_lds + j);
+                    const float* slot = slots + j * SLOT;
+                    const uint64_t start4 = tile.start * 4;
+                    if (!(tile.seg & TAIL_BIT)) {
+#pragma unroll
+                        for (int u = 0; u < U; ++u) {
+                            const uint32_t vi = lane + 64 * u;
+                            if (vi < tile.count)
+                                st32r<4, CPOL_RESIDENT_STORE>(gwrite(a.v) + start4, vi * 16, slot + vi * 4);
+                        }
+                    } else if (lane < tile.count) {
+                        st32r<1, CPOL_RESIDENT_STORE>(gwrite(a.v) + start4, lane * 4, slot + lane);
+                    }
+                }
             }
         }
         if constexpr (MODE == MODE_STEP) {
