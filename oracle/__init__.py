@@ -184,8 +184,8 @@ def step(segs, grads, w, v, lr, mu, wd, batch, order="tree", out=None, bcast=Non
 
 
 def default_threads():
-    """Host threads for step_parallel: OMP_NUM_THREADS when set (the GPU machine
-    sets it to its CPU share), else every core."""
+    """Host threads for step_parallel: OMP_NUM_THREADS when set (a machine
+    shared between jobs sets it to each job's CPU share), else every core."""
     n = os.cpu_count() or 1
     return max(1, min(n, int(os.environ.get("OMP_NUM_THREADS", n))))
 
