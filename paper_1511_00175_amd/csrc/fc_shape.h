@@ -58,7 +58,7 @@ inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128;
 // the tree step, no spill), 1.8x the parameters of LDS alone per round;
 // fp16 replicas in tiles of 1 vector (1 KiB) with batches of 16 and a stack
 // of depth 5 (K < 512; 92 VGPRs), 1.4x.  Measured on MI355X (us per step):
-// VGG-19 K=16 in 8 rounds instead of 14, 1792 vs 1829 on one box, 1831-1836
+// VGG-19 K=16 in 8 rounds instead of 14, 1792 vs 1829 on one machine, 1831-1836
 // vs 1861-1887 on another; AlexNet fp16 K=128 in 5 rounds instead of 6,
 // 2466.9 vs 2500.2 (both builds alternated in one process; 2469 vs 2496 in
 // the parameter-server order).  Not kept: 5 or 6 fp16 tiles, which give
