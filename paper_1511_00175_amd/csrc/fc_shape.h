@@ -63,8 +63,9 @@ inline bool resident_fits_k(int u, int c, int K) { return u == 1 || K / c < 128;
 // 2466.9 vs 2500.2 (both builds alternated in one process; 2469 vs 2496 in
 // the parameter-server order).  Not kept: 5 or 6 fp16 tiles, which give
 // AlexNet 4 rounds, 2497.8 and 2511.3 vs 2469.3 and 2468.9 with 4 tiles
-// (4 rounds are slower whichever way they are reached; the instance with 5
-// is smaller than the one with 6, so code size is not the cause); 12
+// (the tree step's code: 43 KB with 4 tiles, 49 KB with 5, 57 KB with 6,
+// against the 64 KB instruction cache two CUs share; which limit the larger
+// instances hit was not measured); 12
 // unrolled tiles (106 KB of code) and rolled ones (selects that cost load
 // parallelism: AlexNet fp16 in 3 rounds 2571-2576 vs 2523-2529); fp32 tiles
 // of 1 vector with K < 512, 4 per wave: VGG-19-sized K=32 in 10 rounds
