@@ -80,13 +80,16 @@ def test_special_values(fc, K, order, dtype):
 
 @pytest.mark.parametrize("K", [256, 1000, 1024])
 def test_many_workers(fc, K):
-    """K beyond 31 chunks uses the deeper pending-subtree stack."""
+    """K beyond 31 chunks uses the deeper pending-subtree stack, in the
+    default schedule and in the resident kernel (its depth-7 instances)."""
     segs = [(0, 1000, 1, 1), (1024, 37, 1, 1), (1088, 8, 1, 1)]
-    for dtype in ("f32", "f16"):
-        for order in ("tree", "linear"):
-            bad, _, _ = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(K))
-            assert bad == 0, (dtype, order)
-    assert run_steps(fc, segs, K, "f32", "tree", np.random.default_rng(K), steps=1) == 0
+    for opts in (None, dict(schedule=3)):
+        for dtype in ("f32", "f16"):
+            for order in ("tree", "linear"):
+                bad, _, _ = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(K), opts=opts)
+                assert bad == 0, (dtype, order, opts)
+                assert run_steps(fc, segs, K, dtype, order, np.random.default_rng(K), steps=1, opts=opts,
+                                 with_out=True, with_bcast=K == 256) == 0, (dtype, order, opts)
 
 
 def test_fp16_widening_exhaustive(fc):
