@@ -160,19 +160,20 @@ def test_fp16_pair_sums_exhaustive(fc, K, positions, order):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-def test_launch_shape_invariance(fc, dtype):
+@pytest.mark.parametrize("order", ["tree", "linear"])
+def test_launch_shape_invariance(fc, dtype, order):
     """Identical bits for every launch shape (and a capped grid that makes
     blocks loop over tiles) -- the association never depends on it."""
     segs = table(5000, dtype)
     K = 37
     ref = None
     for opts in SHAPES + [dict(max_blocks=7), dict(max_blocks=1, vecs_per_thread=2, kchunk=16)]:
-        bad, got, expect = run_reduce(fc, segs, K, dtype, "tree", np.random.default_rng(5), opts=opts)
+        bad, got, expect = run_reduce(fc, segs, K, dtype, order, np.random.default_rng(5), opts=opts)
         assert bad == 0, opts
         if ref is None:
             ref = got
         assert same_bits(got, ref) == 0
-        assert run_steps(fc, segs, K, dtype, "tree", np.random.default_rng(6), steps=1, opts=opts) == 0, opts
+        assert run_steps(fc, segs, K, dtype, order, np.random.default_rng(6), steps=1, opts=opts) == 0, opts
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
