@@ -185,7 +185,15 @@ class Plan:
         return self._reps(x, "grads", _TORCH_DTYPES[self.dtype])
 
     def close(self):
+        """Free the plan (fc_plan_destroy).  Kernels queued by earlier calls
+        may still read its device tables, so the plan's device is
+        synchronized first; garbage collection of a Plan calls this too."""
         if self.handle:
+            try:
+                import torch
+                torch.cuda.synchronize(self.device)
+            except Exception:
+                pass
             fc_plan_destroy(self.handle)
             self.handle = None
 
