@@ -32,8 +32,10 @@
 // give the same bits):
 //   reduce_kernel   one tile per block; reduce-only, or the fused step
 //   resident_kernel one persistent block per CU: reduce a range of tiles into
-//                   LDS (pure reads), then finish it from LDS (and store the
-//                   broadcast copies one destination at a time)
+//                   LDS and registers (pure reads), then finish it from there:
+//                   w' stored, v' parked and stored after a barrier (or, with
+//                   a broadcast, w' stored to the copies one destination at a
+//                   time)
 //   sgd_kernel      the update from a raw sum (second pass of two)
 //   bcast_kernel    copy one vector into K destinations
 //   resident_bcast_kernel  the same copy on a resident plan: a range of tiles
