@@ -220,10 +220,16 @@ def pin_ragged_segments_and_padding():
 
 # ------------------------------------------------------------------ SGD
 def pin_sgd_golden():
-    """Hand-worked steps with exact dyadic values (tests/golden/sgd_example.txt)."""
+    """Hand-worked steps with exact dyadic values (tests/golden/sgd_example.txt),
+    and with per-segment multipliers (tests/golden/sgd_multipliers_example.txt)."""
     for row in _golden_rows("sgd_example.txt"):
         s, batch, lr, mu, wd, w, v, w1, v1 = [float(t) for t in row]
         wn, vn = oracle.sgd_step([(0, 1)], np.float32([w]), np.float32([v]), np.float32([s]),
+                                 lr, mu, wd, int(batch))
+        assert wn[0] == np.float32(w1) and vn[0] == np.float32(v1), row
+    for row in _golden_rows("sgd_multipliers_example.txt"):
+        s, batch, lr, mu, wd, lm, dm, w, v, w1, v1 = [float(t) for t in row]
+        wn, vn = oracle.sgd_step([(0, 1, lm, dm)], np.float32([w]), np.float32([v]), np.float32([s]),
                                  lr, mu, wd, int(batch))
         assert wn[0] == np.float32(w1) and vn[0] == np.float32(v1), row
 
