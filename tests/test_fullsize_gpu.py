@@ -12,7 +12,7 @@ on every host thread (oracle.step_parallel: one range of elements per thread,
 the same scalar arithmetic for every element).  Every element of w' and v',
 the padding between segments included (which neither side may write), must
 match bit for bit.  GoogLeNet (K = 128 copies, one resident round) and
-VGG-19 (K = 16 copies, 14 rounds) also run steps that keep the raw sum and
+VGG-19 (K = 16 copies, 8 rounds) also run steps that keep the raw sum and
 broadcast w' into the K worker copies: every element of those too.
 """
 import numpy as np
@@ -29,6 +29,18 @@ pytestmark = pytest.mark.gpu
 def fc(device):
     import paper_1511_00175_amd as m
     return m
+
+
+@pytest.fixture(scope="module", autouse=True)
+def release_device_memory():
+    """The full-size inputs take tens of GB: the cached device memory goes back
+    to the driver when this module ends, not when the test process exits."""
+    yield
+    import gc
+    import torch
+    gc.collect()
+    if torch.cuda.is_available():
+        torch.cuda.empty_cache()
 
 
 def host(t):
