@@ -498,7 +498,8 @@ def main():
     # the per-XCD rates of its launches so far, twice, with warm-up steps
     # after each
     balance = None
-    if not args.no_balance and info.schedule == 3:
+    resident = info.schedule in (3, 4)
+    if not args.no_balance and resident:
         for _ in range(2):
             rates = [p.balance() for p in plans]
             for _ in range(max(args.warmup, 2 * len(plans))):
@@ -579,8 +580,9 @@ def main():
     variant = wl.name + ("_linear" if args.order == "linear" else "")
     traffic = read_traffic(variant, dom) if plain else None
     prof_us = read_profile_us(variant, dom) if plain else None
-    sched = {1: "fused", 2: "two-pass", 3: "resident"}.get(info.schedule, str(info.schedule))
-    rk = "resident_kernel" if info.schedule == 3 else "reduce_kernel"
+    sched = {1: "fused", 2: "two-pass", 3: "resident", 4: "resident, one launch"}.get(info.schedule,
+                                                                                      str(info.schedule))
+    rk = "resident_kernel" if resident else "reduce_kernel"
 
     res = {
         "metric": METRIC,

@@ -115,6 +115,16 @@ typedef struct fc_plan fc_plan;
  *   also makes fc_tree_reduce store the sums only after each read phase.
  *   Tiles of 64 lanes x 1 vector with batches of 16 replicas (default), or x 2
  *   vectors with batches of 4 (vecs_per_thread 2, K < 512).
+ * RESIDENT_ONE_LAUNCH: RESIDENT with every round in one launch (the whole
+ *   segment table in one kernel, whatever the plan's size): the persistent
+ *   grid walks all its rounds itself, a block barrier
+ *   between them, so fc_step and fc_tree_reduce are one launch each, and
+ *   fc_broadcast one launch of grid x rounds blocks.  Same tiles, ranges and
+ *   bits as RESIDENT (fc_plan_query reports this value); for a plan of one
+ *   round the launches are the same.  With several rounds it is slower on
+ *   MI355X (VGG-19 K=16 fp32, 8 rounds: 1785-1790 us per step vs 1771 us
+ *   with one launch per round): within one launch the blocks drift apart, so
+ *   one round's writes meet the next round's replica reads.
  * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
  *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
  *   round holds the plan or a parameter's replicas take at least 48 bytes
@@ -124,7 +134,8 @@ typedef enum {
     FC_SCHED_AUTO = 0,
     FC_SCHED_FUSED = 1,
     FC_SCHED_TWO_PASS = 2,
-    FC_SCHED_RESIDENT = 3
+    FC_SCHED_RESIDENT = 3,
+    FC_SCHED_RESIDENT_ONE_LAUNCH = 4
 } fc_schedule;
 
 /* Launch shape.  Results are bit-identical for every allowed setting; the
@@ -297,7 +308,8 @@ typedef struct {
     int block_threads;   /* threads per block of the reduce or step launch */
     int vecs_per_thread;
     int kchunk;
-    int schedule;        /* resolved fc_schedule of fc_step: FUSED, TWO_PASS or RESIDENT */
+    int schedule;        /* resolved fc_schedule of fc_step: FUSED, TWO_PASS, RESIDENT or
+                            RESIDENT_ONE_LAUNCH (only when asked for) */
     uint64_t scratch_bytes; /* device memory the plan owns besides its tables */
     int k_waves;         /* always 1: one wave reduces all K replicas of a lane-vector */
     int lds_bytes;       /* RESIDENT: LDS per block (0 for the other schedules) */

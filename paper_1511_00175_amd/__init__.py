@@ -12,10 +12,10 @@ import weakref
 
 from . import _fc
 from ._fc import (FC_F16, FC_F32, FC_NOALLOC_MAX_ELEMS, FC_ORDER_LINEAR, FC_ORDER_TREE, FC_SCHED_AUTO,  # noqa: F401
-                  FC_SCHED_FUSED, FC_SCHED_RESIDENT, FC_SCHED_TWO_PASS, FcError, fc_broadcast, fc_plan_create,
-                  fc_plan_destroy, fc_plan_query, fc_lr_at, fc_plan_balance, fc_plan_read_timing, fc_plan_set_timing,
-                  fc_read_probe, fc_read_probe_blocks, fc_sgd_step, fc_step, fc_step_noalloc, fc_strerror, fc_train,
-                  fc_tree_reduce, lr_policy)
+                  FC_SCHED_FUSED, FC_SCHED_RESIDENT, FC_SCHED_RESIDENT_ONE_LAUNCH, FC_SCHED_TWO_PASS, FcError,
+                  fc_broadcast, fc_plan_create, fc_plan_destroy, fc_plan_query, fc_lr_at, fc_plan_balance,
+                  fc_plan_read_timing, fc_plan_set_timing, fc_read_probe, fc_read_probe_blocks, fc_sgd_step, fc_step,
+                  fc_step_noalloc, fc_strerror, fc_train, fc_tree_reduce, lr_policy)
 
 __all__ = ["Plan", "FcError", "fc_plan_create", "fc_plan_destroy", "fc_plan_query", "fc_plan_set_timing",
            "fc_plan_read_timing", "fc_plan_balance", "fc_tree_reduce", "fc_sgd_step", "fc_broadcast", "fc_step",
@@ -107,7 +107,8 @@ class Plan:
     order   : "tree" (reduction tree) or "linear" (parameter server).
     opts    : launch shape (block_threads, vecs_per_thread, kchunk,
               max_blocks, k_waves) and fc_step schedule (0 auto, 1 fused,
-              2 two-pass, 3 resident); results do not depend on them.
+              2 two-pass, 3 resident, 4 resident with every round in one
+              launch); results do not depend on them.
     """
 
     _step_cache = None  # {buffer ids: (weak references, signatures, checked pointers)}

@@ -36,7 +36,7 @@ class fc_plan_info(ctypes.Structure):
                 ("rounds", ctypes.c_int)]
 
 
-FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS, FC_SCHED_RESIDENT = 0, 1, 2, 3
+FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS, FC_SCHED_RESIDENT, FC_SCHED_RESIDENT_ONE_LAUNCH = 0, 1, 2, 3, 4
 FC_KERNEL_STEP, FC_KERNEL_REDUCE, FC_KERNEL_SGD, FC_KERNEL_BCAST, FC_KERNEL_KINDS = 0, 1, 2, 3, 4
 KERNEL_NAMES = ("step", "reduce", "sgd", "bcast")
 

@@ -41,6 +41,7 @@ struct fc_plan {
     int* d_ranges = nullptr;         // RESIDENT: tile range of each block (res_grid + 1 entries)
     int res_grid = 0;
     int res_rounds = 0;
+    bool res_one_launch = false;     // every round in one launch (FC_SCHED_RESIDENT_ONE_LAUNCH)
     int res_lds = 0;                 // RESIDENT: LDS bytes per block
     int res_slot = 0;                // RESIDENT: LDS bytes per tile
     int res_in_regs = 0;             // RESIDENT: tiles per block held in registers
@@ -182,14 +183,15 @@ hipError_t launch_reduce(const fc::Shape& sh, int mode, int grid, const fc::Redu
 // One launch per round: the kernel boundary keeps the whole grid in step, so
 // one round's update writes never meet the next round's replica reads
 // (measured on MI355X, VGG-19 K=16 in 14 rounds: 1881 us vs 2076 us with
-// all rounds in one launch).
+// all rounds in one launch).  A plan made for one launch gives the kernel
+// every round: block b then takes range b + grid * round in turn.
 hipError_t launch_resident(fc_plan* p, int mode, const fc::ReduceArgs& r, hipStream_t s) {
     fc::ResidentArgs a{};
     a.r = r;
-    a.rounds = 1;
+    a.rounds = p->res_one_launch ? p->res_rounds : 1;
     a.clock = p->res_record ? p->d_clock : nullptr;
     const size_t lds = static_cast<size_t>(p->res_lds);
-    for (int round = 0; round < p->res_rounds; ++round) {
+    for (int round = 0; round < p->res_rounds; round += a.rounds) {
         a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
         const hipError_t e = p->shape.dtype == FC_F16
                                  ? fc::launch_resident_f16(p->shape, mode, p->res_grid, lds, a, s)
@@ -220,9 +222,9 @@ int validate_opts(const fc_launch_opts* o, fc_dtype gdt, int K, fc::Shape& sh, b
     if (o) {
         // k_waves: one wave reduces all K replicas of its lane-vectors (0 or 1)
         if (o->k_waves < 0 || o->k_waves > 1 || o->max_blocks < 0) return FC_EINVAL;
-        if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_RESIDENT) return FC_EINVAL;
+        if (o->schedule < FC_SCHED_AUTO || o->schedule > FC_SCHED_RESIDENT_ONE_LAUNCH) return FC_EINVAL;
         shape_given = o->block_threads || o->vecs_per_thread || o->kchunk || o->k_waves;
-        if (o->schedule == FC_SCHED_RESIDENT) {
+        if (o->schedule == FC_SCHED_RESIDENT || o->schedule == FC_SCHED_RESIDENT_ONE_LAUNCH) {
             // the resident kernel's tiles: 64 lanes of (1 vector, batches of 16)
             // or (2 vectors, batches of 4).  The plan sets the shape.
             const int ru = o->vecs_per_thread ? o->vecs_per_thread : 1;
@@ -379,6 +381,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     int rc = validate_opts(opts, gdt, K, sh, shape_given);
     if (rc) return rc;
     const int sched_req = opts ? opts->schedule : FC_SCHED_AUTO;
+    const bool res_req = sched_req == FC_SCHED_RESIDENT || sched_req == FC_SCHED_RESIDENT_ONE_LAUNCH;
 
     // RESIDENT: one block per compute unit; each round every block takes a
     // range of 256-element tiles whose raw sums fit the compute unit's LDS
@@ -389,10 +392,10 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
         return FC_EHIP;
     int res_u = 1, res_c = 16;  // the resident tiles' lane vectors and batch
     fc::default_resident_shape(gdt, K, res_u, res_c);
-    if (sched_req == FC_SCHED_RESIDENT && opts->vecs_per_thread) {
+    if (res_req && opts->vecs_per_thread) {
         res_u = opts->vecs_per_thread;
         res_c = opts->kchunk ? opts->kchunk : (res_u == 2 ? 4 : 16);
-    } else if (sched_req == FC_SCHED_RESIDENT && opts->kchunk) {
+    } else if (res_req && opts->kchunk) {
         // a batch alone names single-vector tiles, as validate_opts checks
         res_u = 1;
         res_c = opts->kchunk;
@@ -431,7 +434,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     const uint64_t per_elem = static_cast<uint64_t>(K) * (gdt == FC_F16 ? 2 : 4) + 16;
     const uint64_t step_bytes = n_elems > UINT64_MAX / per_elem ? UINT64_MAX : n_elems * per_elem;
     const bool resident =
-        sched_req == FC_SCHED_RESIDENT ||
+        res_req ||
         (sched_req == FC_SCHED_AUTO && !shape_given &&
          fc::default_resident(K, gdt == FC_F16 ? 2 : 4, static_cast<int64_t>(res_rounds), step_bytes));
     if (resident) {
@@ -511,6 +514,7 @@ int fc_plan_create_ex(fc_plan** plan, const fc_segment* segs, int nseg, int K, i
     if (resident) {
         p->res_grid = res_grid;
         p->res_rounds = static_cast<int>(res_rounds);
+        p->res_one_launch = sched_req == FC_SCHED_RESIDENT_ONE_LAUNCH;
         p->res_lds = static_cast<int>(res_lds);
         p->res_slot = static_cast<int>(slot_bytes);
         p->res_in_regs = static_cast<int>(in_regs);
@@ -578,7 +582,7 @@ int fc_plan_query(const fc_plan* p, fc_plan_info* info) {
     info->block_threads = p->shape.block;
     info->vecs_per_thread = p->shape.vecs;
     info->kchunk = p->shape.kchunk;
-    info->schedule = p->schedule;
+    info->schedule = p->res_one_launch ? FC_SCHED_RESIDENT_ONE_LAUNCH : p->schedule;
     info->scratch_bytes = p->d_sum ? p->extent * sizeof(float) : 0;
     info->k_waves = 1;
     info->lds_bytes = p->schedule == FC_SCHED_RESIDENT ? p->res_lds : 0;
@@ -798,12 +802,15 @@ static int fc_broadcast_body(fc_plan* p, const float* src, float* const* dst, vo
         a.K = p->K;
         rc = launch(p, FC_KERNEL_BCAST, s, [&] {
             if (p->schedule != FC_SCHED_RESIDENT) return fc::launch_bcast(p->shape, p->grid, a, s);
-            // resident plans: the step's ranges, one launch per round
+            // resident plans: the step's ranges, one launch per round, or
+            // all rounds' ranges in one launch of grid x rounds blocks
+            // (block b takes range b of the whole table)
             a.slots = p->res_lds / p->res_slot;
-            for (int round = 0; round < p->res_rounds; ++round) {
+            const int per_launch = p->res_one_launch ? p->res_rounds : 1;
+            for (int round = 0; round < p->res_rounds; round += per_launch) {
                 a.ranges = p->d_ranges + static_cast<size_t>(round) * p->res_grid;
-                const hipError_t e =
-                    fc::launch_resident_bcast(p->shape, p->res_grid, static_cast<size_t>(p->res_lds), a, s);
+                const hipError_t e = fc::launch_resident_bcast(p->shape, p->res_grid * per_launch,
+                                                               static_cast<size_t>(p->res_lds), a, s);
                 if (e != hipSuccess) return e;
             }
             return hipSuccess;

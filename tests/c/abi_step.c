@@ -107,8 +107,9 @@ int main(void) {
     }
 
     int failed = 0;
-    const int schedules[4] = {FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS, FC_SCHED_RESIDENT};
-    for (int si = 0; si < 4; ++si) {
+    const int schedules[5] = {FC_SCHED_AUTO, FC_SCHED_FUSED, FC_SCHED_TWO_PASS, FC_SCHED_RESIDENT,
+                              FC_SCHED_RESIDENT_ONE_LAUNCH};
+    for (int si = 0; si < 5; ++si) {
         fc_launch_opts opts;
         memset(&opts, 0, sizeof opts);
         opts.schedule = schedules[si];
@@ -116,6 +117,12 @@ int main(void) {
         int rc = fc_plan_create_ex(&plan, segs, NSEG, K, FC_F32, FC_ORDER_TREE, &opts);
         if (rc != FC_OK) {
             fprintf(stderr, "c client: fc_plan_create_ex: %s\n", fc_strerror(rc));
+            return 1;
+        }
+        fc_plan_info info;
+        if (fc_plan_query(plan, &info) != FC_OK ||
+            (schedules[si] != FC_SCHED_AUTO && info.schedule != schedules[si])) {
+            fprintf(stderr, "c client: schedule %d: the plan reports schedule %d\n", schedules[si], info.schedule);
             return 1;
         }
         /* one fused step on the device and in the oracle, same inputs */

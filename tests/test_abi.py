@@ -58,7 +58,10 @@ def test_strerror(fcmod):
     ([(0, 16)], 4, 0, {"vecs_per_thread": 1, "kchunk": 4}, -1),   # pair not compiled
     ([(0, 16)], 4, 0, {"vecs_per_thread": 4, "kchunk": 16}, -1),
     ([(0, 16)], 4, 0, {"max_blocks": -1}, -1),
-    ([(0, 16)], 4, 0, {"schedule": 4}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 5}, -1),
+    ([(0, 16)], 4, 0, {"schedule": -1}, -1),
+    ([(0, 16)], 4, 0, {"schedule": 4, "vecs_per_thread": 4}, -1),   # one launch: the resident shapes
+    ([(0, 16)], 512, 0, {"schedule": 4, "vecs_per_thread": 2}, -1),
     ([(0, 16)], 4, 0, {"schedule": 3, "k_waves": 4}, -1),        # resident: one launch shape
     ([(0, 16)], 4, 0, {"schedule": 3, "vecs_per_thread": 4}, -1),
     ([(0, 16)], 4, 0, {"schedule": 3, "block_threads": 128}, -1),

@@ -178,12 +178,13 @@ def test_launch_shape_invariance(fc, dtype, order):
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
 @pytest.mark.parametrize("order", ["tree", "linear"])
-@pytest.mark.parametrize("schedule", [1, 2, 3])
+@pytest.mark.parametrize("schedule", [1, 2, 3, 4])
 @pytest.mark.parametrize("K", [3, 64, 130])
 def test_schedules_match_oracle(fc, K, schedule, order, dtype):
     """fc_step in one fused pass, in two passes (raw sum, then update) and
-    resident, with and without the raw sum and the broadcast, over chained
-    steps, in both orders."""
+    resident (one launch per round, or every round in one launch), with and
+    without the raw sum and the broadcast, over chained steps, in both
+    orders."""
     segs = table(9000 + K, dtype, nseg=5, max_len=3000)
     rng = np.random.default_rng(K + schedule)
     for with_out, with_bcast in ((False, False), (True, False), (False, True), (True, True)):
@@ -318,13 +319,14 @@ def test_fused_equals_composed(fc):
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
 @pytest.mark.parametrize("schedule,max_blocks,vecs", [(0, 0, 0), (1, 0, 0), (2, 0, 0), (3, 0, 1), (3, 0, 2),
-                                                      (3, 1, 1), (3, 1, 2), (3, 2, 1)])
+                                                      (3, 1, 1), (3, 1, 2), (3, 2, 1), (4, 1, 1), (4, 2, 2)])
 @pytest.mark.parametrize("K", [1, 5, 40])
 def test_broadcast_matches_oracle(fc, K, schedule, max_blocks, vecs, dtype):
     """fc_broadcast on each schedule's tile map: on resident plans one
     persistent block per CU stages its range of the source in LDS and stores
-    it one destination at a time (one round, or many with few blocks); on the
-    others one block per tile.  Every destination gets the source's bits on
+    it one destination at a time (one round, or many with few blocks, one
+    launch per round or all rounds' blocks in one launch); on the others one
+    block per tile.  Every destination gets the source's bits on
     every segment element (special values included) and keeps its fill
     value elsewhere; the replica type only changes the plan's tile map."""
     import torch
@@ -337,8 +339,8 @@ def test_broadcast_matches_oracle(fc, K, schedule, max_blocks, vecs, dtype):
     if vecs:
         opts["vecs_per_thread"] = vecs
     plan = fc.Plan(segs, K, dtype, "tree", **opts)
-    if schedule == 3 and max_blocks:
-        assert plan.info().rounds > 1
+    if schedule in (3, 4) and max_blocks:
+        assert (plan.info().schedule, plan.info().rounds > 1) == (schedule, True)
     dst = torch.full((K, n), -2.0, device="cuda")
     plan.broadcast(to_dev(src), dst)
     torch.cuda.synchronize()
@@ -430,7 +432,7 @@ def test_empty_and_zero_length(fc):
 
 
 @pytest.mark.parametrize("K,dtype,schedule,max_blocks", [(4, "f32", 1, 0), (130, "f32", 2, 0), (16, "f16", 1, 0),
-                                                         (128, "f32", 0, 0), (40, "f32", 3, 1)])
+                                                         (128, "f32", 0, 0), (40, "f32", 3, 1), (40, "f32", 4, 1)])
 def test_graph_capture_replays(fc, K, dtype, schedule, max_blocks):
     """A step whose pointer tables are already on the device, called on the
     stream it last ran on, enqueues kernel launches only, so it can be
@@ -507,19 +509,22 @@ def test_resident_matches_oracle(fc, K, max_blocks, vecs, dtype, order):
                      with_bcast=K <= 64) == 0
 
 
+@pytest.mark.parametrize("schedule", [3, 4])
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
 @pytest.mark.parametrize("K,max_blocks,vecs", [(5, 1, 1), (33, 2, 1), (130, 1, 1), (40, 1, 2)])
-def test_resident_rounds_match_oracle(fc, K, max_blocks, vecs, dtype):
+def test_resident_rounds_match_oracle(fc, K, max_blocks, vecs, dtype, schedule):
     """A plan larger than the grid's LDS takes several rounds (here with 1-3
-    blocks of 160 tile slots each); every round's ranges are finished before
-    the next round's reduce reuses the slots."""
+    blocks of 160 tile slots each), one launch per round or all of them in
+    one launch; every round's ranges are finished before the next round's
+    reduce reuses the slots."""
     rows = [(0, 50000, 1, 1), (50048, 7, 2.0, 0.0), (50112, 60001, 1, 1), (110144, 200000, 1, 1)]
-    p = fc.Plan(rows, K, dtype, "tree", schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    p = fc.Plan(rows, K, dtype, "tree", schedule=schedule, max_blocks=max_blocks, vecs_per_thread=vecs)
     info = p.info()
     p.close()
     assert info.rounds >= 2 and info.grid == max_blocks and info.vecs_per_thread == vecs
+    assert info.schedule == schedule
     rng = np.random.default_rng(K)
-    opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    opts = dict(schedule=schedule, max_blocks=max_blocks, vecs_per_thread=vecs)
     bad, _, _ = run_reduce(fc, rows, K, dtype, "tree", rng, opts=opts)
     assert bad == 0
     assert run_steps(fc, rows, K, dtype, "tree", rng, steps=2, opts=opts, with_out=True) == 0
@@ -633,17 +638,19 @@ def test_sharded_reduction_equals_full_tree(fc, K, S):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
-@pytest.mark.parametrize("K,max_blocks,vecs", [(16, 8, 1), (33, 16, 1), (5, 1, 1), (64, 3, 1), (40, 2, 2)])
-def test_balance_keeps_bits(fc, K, max_blocks, vecs, dtype):
+@pytest.mark.parametrize("K,max_blocks,vecs,schedule", [(16, 8, 1, 3), (33, 16, 1, 3), (5, 1, 1, 3), (64, 3, 1, 3),
+                                                        (40, 2, 2, 3), (5, 1, 1, 4), (40, 2, 2, 4)])
+def test_balance_keeps_bits(fc, K, max_blocks, vecs, schedule, dtype):
     """fc_plan_balance after every step re-divides the resident tiles among
     the blocks by their XCDs' measured rates: every step before and after
     stays bit-exact with the oracle (update, raw sum, and for K <= 16 the
     broadcast copies), in one round over 8 or 16 blocks (every XCD) and in
-    several rounds (1-3 blocks of 160 tile slots); so does fc_broadcast on
-    the rebalanced ranges."""
+    several rounds (1-3 blocks of 160 tile slots; one launch per round or
+    all rounds in one launch, whose blocks add up their rounds' record); so
+    does fc_broadcast on the rebalanced ranges."""
     segs = table(16000 + K, dtype, nseg=9)
     segs = segs + [(alloc_len(segs), 300000, 1.0, 1.0)]  # >= 32 tiles per block: launches record
-    opts = dict(schedule=3, max_blocks=max_blocks, vecs_per_thread=vecs)
+    opts = dict(schedule=schedule, max_blocks=max_blocks, vecs_per_thread=vecs)
     p = fc.Plan(segs, K, dtype, "tree", **opts)
     info = p.info()
     assert p.balance() == [0.0] * 16  # nothing launched yet: no change, no rates
