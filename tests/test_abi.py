@@ -151,3 +151,43 @@ def test_header_is_plain_c(tmp_path):
     r = subprocess.run(["gcc", "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-fsyntax-only",
                         f"-I{os.path.join(ROOT, 'include')}", str(src)], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_binding_matches_header(tmp_path, fcmod):
+    """Every constant the header defines has the same value in the binding,
+    and every structure the binding passes has the header's size and field
+    offsets (a C program built with gcc reports the header's view)."""
+    import subprocess
+    f = fcmod._fc
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    consts = sorted(set(re.findall(r"\b(FC_[A-Z0-9_]+)\s*(?:=|\(|[0-9])", text)) - {"FC_H"})
+    consts = [c for c in consts if re.search(rf"(#define\s+{c}\b|\b{c}\s*=)", text)]
+    assert "FC_SCHED_RESIDENT_ONE_LAUNCH" in consts and "FC_NOALLOC_MAX_ELEMS" in consts
+    structs = {name: [fname for fname, _ in getattr(f, name)._fields_]
+               for name in ("fc_segment", "fc_launch_opts", "fc_plan_info", "fc_timing", "fc_lr_policy")}
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "fc.h"', "int main(void) {"]
+    lines += [f'    printf("{c} %lld\\n", (long long)({c}));' for c in consts]
+    for s, fields in structs.items():
+        lines.append(f'    printf("sizeof {s} %zu\\n", sizeof({s}));')
+        lines += [f'    printf("offsetof {s}.{fl} %zu\\n", offsetof({s}, {fl}));' for fl in fields]
+    lines += ["    return 0;", "}"]
+    src = tmp_path / "abi_view.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "abi_view"
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", f"-I{os.path.join(ROOT, 'include')}", str(src),
+                        "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines()
+    seen = 0
+    for line in out:
+        key, val = line.rsplit(" ", 1)
+        val = int(val)
+        if key.startswith("sizeof "):
+            assert ctypes.sizeof(getattr(f, key.split()[1])) == val, key
+        elif key.startswith("offsetof "):
+            s, fl = key.split()[1].split(".")
+            assert getattr(getattr(f, s), fl).offset == val, key
+        else:
+            assert getattr(f, key) == val, key
+        seen += 1
+    assert seen == len(consts) + sum(1 + len(v) for v in structs.values())
