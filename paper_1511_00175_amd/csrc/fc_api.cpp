@@ -38,7 +38,7 @@ struct fc_plan {
     float** d_dst = nullptr;         // K broadcast pointers
     float* d_sum = nullptr;          // raw-sum scratch of the two-pass schedule (extent floats)
     int schedule = FC_SCHED_FUSED;   // resolved schedule of fc_step
-    int* d_ranges = nullptr;         // RESIDENT: tile range of each block (res_grid + 1 entries)
+    int* d_ranges = nullptr;         // RESIDENT: tile range of each block in each round (res_grid * res_rounds + 1)
     int res_grid = 0;
     int res_rounds = 0;
     bool res_one_launch = false;     // every round in one launch (FC_SCHED_RESIDENT_ONE_LAUNCH)
