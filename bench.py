@@ -361,6 +361,40 @@ def graph_steps(plan, wl, inputs, out, bcast, n):
             "value": round(wl.algorithmic_bytes() / us / 1e3, 2), "input_sets": 1}
 
 
+def train_steps(plan, wl, inputs, n):
+    """fc_train over n iterations of a poly learning-rate policy (power 0.5,
+    the paper's GoogLeNet schedule, Sec. 7.3) on one input set, against a
+    Python loop of n fc_step calls at the base rate on the same buffers; µs
+    per iteration from HIP events on the current stream, best of 3."""
+    import torch
+
+    r, w, v = inputs
+    policy = dict(kind="poly", base_lr=wl.lr, max_iter=n, power=0.5)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) * 1e3 / n)
+        return best
+
+    def loop():
+        for _ in range(n):
+            plan.step(r, w, v, wl.lr, wl.mu, wl.wd, wl.batch)
+
+    us_train = timed(lambda: plan.train(r, w, v, policy, 0, n, wl.mu, wl.wd, wl.batch))
+    us_loop = timed(loop)
+    return {"iters": n, "policy": policy, "us_per_iter": round(us_train, 2),
+            "value": round(wl.algorithmic_bytes() / us_train / 1e3, 2),
+            "step_loop_us_per_iter": round(us_loop, 2), "input_sets": 1}
+
+
 def bandwidth_probes(dev):
     """Bandwidth ceilings measured on this GPU: the library's streaming read
     probe over 4 GiB, and torch's device copy of 1 GiB (1 GiB read + 1 GiB
@@ -425,6 +459,9 @@ def main():
     ap.add_argument("--graph", type=int, default=0,
                     help="also capture this many steps (one input set) in one HIP graph and report the "
                          "graph-amortized time per step")
+    ap.add_argument("--train-iters", type=int, default=0,
+                    help="also time fc_train (poly learning-rate policy) over this many iterations on one input "
+                         "set, beside a Python loop of fc_step calls on the same buffers")
     ap.add_argument("--no-probes", action="store_true",
                     help="skip the read and copy bandwidth probes reported beside the roofline")
     ap.add_argument("--no-balance", action="store_true",
@@ -546,6 +583,9 @@ def main():
     graph = None
     if args.graph > 0:
         graph = graph_steps(plan, wl, sets[0], out, bcast, args.graph)
+    train = None
+    if args.train_iters > 0:
+        train = train_steps(plan, wl, sets[0], args.train_iters)
     for _ in range(args.profile_loop):
         step()
     torch.cuda.synchronize()
@@ -649,6 +689,8 @@ def main():
                                           "frac": round(model_us / (ms_per_step * 1e3), 4)}
     if graph:
         res["graph"] = graph
+    if train:
+        res["train"] = train
     res["parity"] = None
     host_copies = None
     if not args.no_parity:

@@ -15,9 +15,10 @@ pytestmark = pytest.mark.gpu
 def test_bench_line_carries_parity(device):
     """A short run on the flat workload (one fused kernel per step): the line
     reports every element of w' and v' checked against the oracle, none
-    differing, and the exit status is 0."""
+    differing, and the exit status is 0; the multi-step driver is timed beside
+    the step loop."""
     r = subprocess.run([sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", "flat", "--steps", "5",
-                        "--warmup", "2", "--no-probes", "--cpu-seconds", "0.2"],
+                        "--warmup", "2", "--no-probes", "--cpu-seconds", "0.2", "--train-iters", "10"],
                        capture_output=True, text=True, cwd=ROOT, timeout=240)
     assert r.returncode == 0, r.stderr[-2000:]
     line = json.loads(r.stdout.strip().splitlines()[-1])
@@ -25,6 +26,9 @@ def test_bench_line_carries_parity(device):
     assert par["bit_exact"] and par["mismatches"] == 0
     assert par["elements"] == 2 * (1 << 20) and par["outputs"] == ["w", "v"]
     assert line["cpu_baseline"]["cores"] >= 1 and line["roofline"]["call_us_avg"] > 0
+    tr = line["train"]
+    assert tr["iters"] == 10 and tr["policy"]["kind"] == "poly"
+    assert tr["us_per_iter"] > 0 and tr["step_loop_us_per_iter"] > 0
 
 
 def test_sweep_k_errors_within_bounds(device):
