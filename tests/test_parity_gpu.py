@@ -474,6 +474,19 @@ def test_graph_capture_replays(fc, K, dtype, schedule, max_blocks):
     pb.close()
 
 
+def test_calls_default_to_torchs_current_stream(fc):
+    """Without a stream argument a call runs on torch's current stream of the
+    current device, also inside a stream context."""
+    import torch
+    from paper_1511_00175_amd import _stream
+    assert _stream(None) == torch.cuda.current_stream().cuda_stream
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        assert _stream(None) == s.cuda_stream == torch.cuda.current_stream().cuda_stream
+    assert _stream(None) == torch.cuda.current_stream().cuda_stream
+    assert _stream(s) == s.cuda_stream and _stream(s.cuda_stream) == s.cuda_stream
+
+
 def test_read_probe_reads_every_byte(fc):
     """The probe's per-block sums of an all-ones buffer count its floats
     exactly (a ragged last block included)."""
