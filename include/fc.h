@@ -144,8 +144,9 @@ typedef enum {
  * RESIDENT -> 64-lane tiles of (2 vectors, batches of 4 replicas) for fp32
  * replicas with K <= 16, else (1 vector, batches of 16); vecs_per_thread and
  * kchunk may name either; otherwise fp16 -> (4 vectors, 4 replicas, 256
- * threads); fp32 with 16 < K <= 64 -> (4, 2, 256); other fp32 -> (1, 16,
- * 64).  Replica loads always carry the streaming (nt) hint. */
+ * threads); fp32 with K <= 4 -> (1, 8, 256); fp32 with 16 < K <= 64 ->
+ * (4, 2, 256); other fp32 -> (1, 16, 64).  Replica loads always carry the
+ * streaming (nt) hint. */
 typedef struct {
     int block_threads;   /* 64, 128 or 256 threads per block */
     int vecs_per_thread; /* 4-element lane-vectors per thread (1, 2 or 4) ... */

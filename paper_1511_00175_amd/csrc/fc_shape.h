@@ -13,14 +13,23 @@ namespace fc {
 
 // Launch-shape defaults, measured on MI355X for the five workloads:
 //   fp16 replicas       : 4 vectors per lane, 4 replicas per batch, 256 threads
+//   fp32, K <= 4        : 1 vector per lane, 8 replicas per batch, 256 threads
 //   fp32, 16 < K <= 64  : 4 vectors per lane, 2 replicas per batch, 256 threads
 //   other fp32          : 1 vector per lane, 16 replicas per batch, 64 threads
 // Four vectors per lane make every wave read 4 KiB of one replica at a time,
 // which HBM serves better than 1 KiB pieces, as long as the lane's registers
 // (16 accumulators per pending subtree) still allow enough waves in flight.
+// With at most 4 replicas a step is short and launch-bound: 4x fewer,
+// larger blocks and a batch no larger than needed measured (2^20 parameters,
+// us per step, steps with w, v from HBM / 20-step HIP graph on one set,
+// against (1, 16, 64)): K=4 6.98-7.04 / 4.67-5.12 vs 7.58-7.79 / 4.79-5.10,
+// K=2 5.78 / 4.39 vs 5.98 / 4.59; from K=8 on no better (K=8 10.68 / 7.66
+// vs 10.55 / 8.09, K=16 16.47 / 14.44 vs 15.37 / 14.43).
 inline void default_shape(fc_dtype gdt, int K, fc::Shape& sh) {
     if (gdt == FC_F16) {
         sh.vecs = 4; sh.kchunk = 4; sh.block = 256;
+    } else if (K <= 4) {
+        sh.vecs = 1; sh.kchunk = 8; sh.block = 256;
     } else if (K > 16 && K <= 64) {
         sh.vecs = 4; sh.kchunk = 2; sh.block = 256;
     } else {
