@@ -433,6 +433,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup-seconds", type=float, default=3.0,
+                    help="warm up for at least this long as well as for --warmup steps")
     ap.add_argument("--workload", default="googlenet",
                     choices=["flat", "nin", "googlenet", "vgg19", "alexnet", "googlenet_aux", "googlenet_caffe_bias",
                              "alexnet_ungrouped"])
@@ -528,8 +530,15 @@ def main():
         count[0] += 1
         plans[i].step(sets[i][0], ww, vv, wl.lr, wl.mu, wl.wd, wl.batch, out=out, bcast=bcast)
 
-    for _ in range(args.warmup):
+    # warm-up: at least W steps and at least --warmup-seconds of back-to-back
+    # steps (a process started within seconds of another process freeing tens
+    # of GB of device memory runs its first second or two about 4% slower)
+    warm_steps, t_warm = 0, time.perf_counter()
+    while warm_steps < args.warmup or time.perf_counter() - t_warm < args.warmup_seconds:
         step()
+        warm_steps += 1
+        if warm_steps % 20 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     # XCD-aware shares (resident schedule): each plan re-divides its tiles by
     # the per-XCD rates of its launches so far, twice, with warm-up steps
@@ -631,6 +640,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm_steps,
         "ms_per_step": round(ms_per_step, 4),
         "us_per_step": round(ms_per_step * 1e3, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
