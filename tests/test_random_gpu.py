@@ -58,3 +58,37 @@ def test_random_configuration_matches_oracle(fc, seed):
     assert bad == 0, case
     assert run_steps(fc, rows, K, dtype, order, rng, steps=2, opts=opts, with_out=with_out, with_bcast=with_bcast,
                      special=special) == 0, case
+
+
+@pytest.mark.parametrize("seed", range(1000, 1064))
+def test_random_composed_step_matches_oracle(fc, seed):
+    """The step composed from the boundary's separate calls -- fc_tree_reduce,
+    then fc_sgd_step from that raw sum, then fc_broadcast of w' -- on the
+    same random configurations: w', v' and every copy equal the oracle's
+    fused step."""
+    import torch
+    import oracle
+    from gpu_cases import LR, MU, WD, host_replicas, same_bits, to_dev
+    rows, K, dtype, order, opts, _, _, special = draw(seed)
+    K = min(K, 64)  # K broadcast copies
+    print(f"case {seed}: K={K} {dtype} {order} {opts} nseg={len(rows)}", flush=True)
+    rng = np.random.default_rng(20_000 + seed)
+    n = alloc_len(rows)
+    npdt = np.float16 if dtype == "f16" else np.float32
+    reps = host_replicas(rng, K, n, npdt, scale=0.01, special=special)
+    w = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+    v = rng.standard_normal(n, dtype=np.float32) * np.float32(0.001)
+    dst_h = [np.full(n, -2.0, np.float32) for _ in range(K)]
+    ew, ev, _, _ = oracle.step(rows, list(reps), w.copy(), v.copy(), LR, MU, WD, 256, order=order, bcast=dst_h)
+    plan = fc.Plan(rows, K, dtype, order, **opts)
+    w_d, v_d, g_d = to_dev(w), to_dev(v), torch.zeros(n, device="cuda")
+    dst_d = torch.full((K, n), -2.0, device="cuda")
+    plan.tree_reduce(to_dev(reps), g_d)
+    plan.sgd_step(w_d, v_d, g_d, LR, MU, WD, 256)
+    plan.broadcast(w_d, dst_d)
+    torch.cuda.synchronize()
+    plan.close()
+    assert same_bits(w_d.cpu().numpy(), ew) == 0
+    assert same_bits(v_d.cpu().numpy(), ev) == 0
+    got = dst_d.cpu().numpy()
+    assert sum(same_bits(got[k], dst_h[k]) for k in range(K)) == 0
