@@ -92,3 +92,40 @@ def test_random_composed_step_matches_oracle(fc, seed):
     assert same_bits(v_d.cpu().numpy(), ev) == 0
     got = dst_d.cpu().numpy()
     assert sum(same_bits(got[k], dst_h[k]) for k in range(K)) == 0
+
+
+@pytest.mark.parametrize("seed", range(2000, 2032))
+def test_random_step_noalloc_matches_oracle(fc, seed):
+    """fc_step_noalloc (the step in two passes with the raw sum in the
+    library's fixed device array) on seeded random configurations, two
+    chained steps of shrinking size: w', v' and the optional outputs equal
+    the oracle's."""
+    import torch
+    import oracle
+    from gpu_cases import LR, MU, WD, host_replicas, same_bits, to_dev
+    rows, K, dtype, order, opts, with_out, with_bcast, special = draw(seed)
+    print(f"case {seed}: K={K} {dtype} {order} {opts} nseg={len(rows)} out={with_out} bcast={with_bcast}",
+          flush=True)
+    rng = np.random.default_rng(30_000 + seed)
+    npdt = np.float16 if dtype == "f16" else np.float32
+    for table in (rows, rows[:max(1, len(rows) // 2)]):
+        n = alloc_len(table)
+        reps = host_replicas(rng, K, n, npdt, scale=0.01, special=special)
+        w = rng.standard_normal(n, dtype=np.float32) * np.float32(0.05)
+        v = np.zeros(n, np.float32)
+        out_h = np.full(n, -1.0, np.float32) if with_out else None
+        dst_h = [np.full(n, -2.0, np.float32) for _ in range(K)] if with_bcast else None
+        ew, ev, _, _ = oracle.step(table, list(reps), w, v, LR, MU, WD, 256, order=order, out=out_h, bcast=dst_h)
+        plan = fc.Plan(table, K, dtype, order, **opts)
+        w_d, v_d = to_dev(w), to_dev(v)
+        out_d = torch.full((n,), -1.0, device="cuda") if with_out else None
+        dst_d = torch.full((K, n), -2.0, device="cuda") if with_bcast else None
+        plan.step_noalloc(to_dev(reps), w_d, v_d, LR, MU, WD, 256, out=out_d, bcast=dst_d)
+        torch.cuda.synchronize()
+        plan.close()
+        assert same_bits(w_d.cpu().numpy(), ew) == 0 and same_bits(v_d.cpu().numpy(), ev) == 0
+        if with_out:
+            assert same_bits(out_d.cpu().numpy(), out_h) == 0
+        if with_bcast:
+            got = dst_d.cpu().numpy()
+            assert sum(same_bits(got[k], dst_h[k]) for k in range(K)) == 0
