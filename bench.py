@@ -313,6 +313,110 @@ def sweep_k(n, ks=FIG4_KS, reps_per_k=20, seed=1511, samples=1 << 16):
     return recs
 
 
+XGMI_LINK_GBS = 153.0  # one MI355X xGMI link, per direction (7 links per GPU)
+
+
+def _mean_call_us(plan, kind, fn, n):
+    """Mean duration of a call kind over n calls (the library's HIP events)."""
+    import torch
+
+    plan.set_timing(True)
+    fn()
+    torch.cuda.synchronize()
+    plan.read_timing()
+    for _ in range(n):
+        fn()
+    torch.cuda.synchronize()
+    launches, total = plan.read_timing()[kind]
+    plan.set_timing(False)
+    return total / launches
+
+
+def shard_share(wl, G, seed=1511, reps=20):
+    """One GPU's share of the step when G GPUs split the K workers into G
+    aligned runs of S = K/G (one subtree each) and the parameters into G
+    slices, measured on this GPU at the real per-GPU shapes; the exchange
+    between GPUs is not built, its time is modelled from the xGMI link rate.
+      leaf : fc_tree_reduce over this GPU's S workers for all N parameters
+             (its subtree's partial sums, written once);
+      owner: fc_step on this GPU's slice with the G subtree partials as its
+             workers (the top of the tree, the average, SGD).
+    Parity: all G leaf reduces and all G owner steps run here, and every
+    element of the sharded w', v' is compared bit for bit with the oracle's
+    one-GPU step on the same inputs (reducing aligned runs of 2^m leaves and
+    then the run sums in order is the tree over all K leaves, Sec. 6.2)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_1511_00175_amd as fc
+    from workloads import gen
+
+    K = wl.K
+    S = K // G
+    if G < 1 or K % G or S & (S - 1):
+        raise SystemExit(f"bench.py: --shard {G} must divide K={K} into runs of a power of two")
+    dev = torch.device("cuda:0")
+    reps_d, w0, v0 = gen.device_inputs(wl, seed, dev)
+    table = wl.table()
+    ext = max(o + n for o, n, _, _ in table)
+    bounds = [min(ext, (r * ext // G) // 64 * 64) for r in range(G)] + [ext]
+
+    def clip(a, b):
+        return [(max(o, a), min(o + n, b) - max(o, a), lr, dm) for o, n, lr, dm in table if min(o + n, b) > max(o, a)]
+
+    # the leaves: G subtree partial sums, each a full-length fp32 vector
+    leaf = fc.Plan(table, S, wl.dtype, "tree")
+    parts = torch.zeros((G, wl.padded), device=dev)
+    for k in range(G):
+        leaf.tree_reduce(reps_d[k * S:(k + 1) * S], parts[k])
+    torch.cuda.synchronize()
+    leaf_us = _mean_call_us(leaf, "reduce", lambda: leaf.tree_reduce(reps_d[:S], parts[0]), reps)
+    for k in range(G):  # the timed calls rewrote partial 0 with the same values
+        leaf.tree_reduce(reps_d[k * S:(k + 1) * S], parts[k])
+    leaf.close()
+    # the owners: one plan per slice over the G partials; every slice stepped once
+    w_s, v_s = w0.clone(), v0.clone()
+    owners = [fc.Plan(clip(bounds[r], bounds[r + 1]), G, "f32", "tree") for r in range(G)]
+    for r in range(G):
+        owners[r].step(parts, w_s, v_s, wl.lr, wl.mu, wl.wd, wl.batch)
+    torch.cuda.synchronize()
+    w_t, v_t = w0.clone(), v0.clone()
+    owner_us = _mean_call_us(owners[0], "step",
+                             lambda: owners[0].step(parts, w_t, v_t, wl.lr, wl.mu, wl.wd, wl.batch), reps)
+    slice_params = sum(n for _, n, _, _ in clip(bounds[0], bounds[1]))
+    for p in owners:
+        p.close()
+    # the whole step on one GPU, for comparison
+    full = fc.Plan(table, K, wl.dtype, "tree")
+    w_f, v_f = w0.clone(), v0.clone()
+    one_us = _mean_call_us(full, "step", lambda: full.step(reps_d, w_f, v_f, wl.lr, wl.mu, wl.wd, wl.batch), reps)
+    full.close()
+    # parity of the sharded step against the oracle's one-GPU step
+    threads = oracle.default_threads()
+    ew, ev, _, _ = oracle.step_parallel(table, reps_d.cpu().numpy(), w0.cpu().numpy(), v0.cpu().numpy(), wl.lr, wl.mu,
+                                        wl.wd, wl.batch, threads=threads)
+    bad = mismatches(w_s.cpu().numpy(), ew) + mismatches(v_s.cpu().numpy(), ev)
+    slice_bytes = 4 * (bounds[1] - bounds[0])
+    rs_us = slice_bytes / (XGMI_LINK_GBS * 1e3)  # 7 foreign slices out and in, one per link, at once
+    ag_us = slice_bytes / (XGMI_LINK_GBS * 1e3)  # w' slice to the 7 peers, one per link
+    per_gpu = leaf_us + rs_us + owner_us + ag_us
+    return {"shard": G, "workload": f"{wl.name}_k{K}_{wl.dtype}", "workers_per_gpu": S, "n_params": wl.n_params,
+            "slice_params": slice_params,
+            "leaf_reduce_us": round(leaf_us, 2),
+            "leaf_gb_s": round((S * wl.s_g + 4) * wl.n_params / leaf_us / 1e3, 1),
+            "owner_step_us": round(owner_us, 2),
+            "exchange_model_us": {"reduce_scatter": round(rs_us, 2), "all_gather": round(ag_us, 2),
+                                  "link_gb_s": XGMI_LINK_GBS, "bytes_per_link": slice_bytes},
+            "per_gpu_step_us": round(per_gpu, 2), "one_gpu_step_us": round(one_us, 2),
+            "step_speedup_model": round(one_us / per_gpu, 2),
+            "parity": {"bit_exact": bad == 0, "elements": 2 * w_s.numel(), "mismatches": bad,
+                       "checked": "every element of the sharded w', v' (all G slices' owner steps) against the "
+                                  "oracle's one-GPU step on the same inputs"},
+            "timing": "mean of the library's HIP events over the calls; the owner's G partial slices and w, v "
+                      "slice fit the Infinity Cache"}
+
+
 def input_hash(sets, wv):
     """sha256 (first 16 hex digits) over the first and last 4 KiB of every
     input buffer (each replica row of every replica set, then w and v of
@@ -456,6 +560,9 @@ def main():
     ap.add_argument("--sweep-k", action="store_true",
                     help="instead of the benchmark line, print the tree vs parameter-server K sweep")
     ap.add_argument("--sweep-reps", type=int, default=20)
+    ap.add_argument("--shard", type=int, default=0,
+                    help="instead of the benchmark line, measure one GPU's share of the step on G GPUs "
+                         "(leaf reduce + owner step, exchange modelled) and check the sharded result's bits")
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="do not record per-kernel events (roofline entry then uses the wall time per step)")
     ap.add_argument("--graph", type=int, default=0,
@@ -500,6 +607,13 @@ def main():
         return
     dev = torch.device("cuda:0")
     wl = tables.get(args.workload)
+    if args.shard:
+        rec = shard_share(wl, args.shard, seed=args.seed)
+        rec["kernel_source_sha256_16"] = kernel_hash()
+        print(json.dumps(rec), flush=True)
+        if not rec["parity"]["bit_exact"]:
+            sys.exit(1)
+        return
     opts = {}
     for kv in filter(None, args.opts.split(",")):
         k, v = kv.split("=")

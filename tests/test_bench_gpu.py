@@ -53,3 +53,16 @@ def test_sweep_k_errors_within_bounds(device):
     by = {(r["K"], r["order"]): r for r in recs}
     for K in ks:
         assert by[(K, "tree")]["bound_gamma_d"] <= by[(K, "linear")]["bound_gamma_d"]
+
+
+def test_shard_share_is_bit_exact(device):
+    """--shard 8 on NiN (32 workers: 8 subtrees of 4): the leaf reduces and the
+    owners' steps over the 8 subtree partials reproduce the oracle's one-GPU
+    step on every element, and each part of one GPU's share is timed."""
+    r = subprocess.run([sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", "nin", "--shard", "8"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    rec = json.loads(r.stdout.strip().splitlines()[-1])
+    assert rec["shard"] == 8 and rec["workers_per_gpu"] == 4
+    assert rec["parity"]["bit_exact"] and rec["parity"]["mismatches"] == 0
+    assert rec["leaf_reduce_us"] > 0 and rec["owner_step_us"] > 0 and rec["per_gpu_step_us"] > rec["leaf_reduce_us"]
