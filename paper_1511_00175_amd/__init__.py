@@ -62,8 +62,12 @@ def _stream(stream):
         return int(stream) if not hasattr(stream, "cuda_stream") else stream.cuda_stream
     if _CURRENT_STREAM is None:
         import torch
-        raw, dev = torch._C._cuda_getCurrentRawStream, torch._C._cuda_getDevice
-        _CURRENT_STREAM = lambda: raw(dev())  # noqa: E731
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        dev = getattr(torch._C, "_cuda_getDevice", None)
+        if raw is not None and dev is not None:
+            _CURRENT_STREAM = lambda: raw(dev())  # noqa: E731
+        else:  # a torch without the raw accessors: the public, slower call
+            _CURRENT_STREAM = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
     return _CURRENT_STREAM()
 
 
