@@ -332,6 +332,17 @@ def _mean_call_us(plan, kind, fn, n):
     return total / launches
 
 
+def shard_tables(table, G):
+    """The G owners' segment tables: the element range [0, extent) cut at
+    multiples of 64 elements into G slices, each segment clipped to each
+    slice (offsets stay those of the full buffers).  Every segment element
+    lies in exactly one slice's table, with its segment's multipliers."""
+    ext = max((o + n for o, n, _, _ in table), default=0)
+    bounds = [min(ext, (r * ext // G) // 64 * 64) for r in range(G)] + [ext]
+    return [[(max(o, a), min(o + n, b) - max(o, a), lr, dm) for o, n, lr, dm in table if min(o + n, b) > max(o, a)]
+            for a, b in zip(bounds[:-1], bounds[1:])], bounds
+
+
 def shard_share(wl, G, seed=1511, reps=20):
     """One GPU's share of the step when G GPUs split the K workers into G
     aligned runs of S = K/G (one subtree each) and the parameters into G
@@ -359,11 +370,7 @@ def shard_share(wl, G, seed=1511, reps=20):
     dev = torch.device("cuda:0")
     reps_d, w0, v0 = gen.device_inputs(wl, seed, dev)
     table = wl.table()
-    ext = max(o + n for o, n, _, _ in table)
-    bounds = [min(ext, (r * ext // G) // 64 * 64) for r in range(G)] + [ext]
-
-    def clip(a, b):
-        return [(max(o, a), min(o + n, b) - max(o, a), lr, dm) for o, n, lr, dm in table if min(o + n, b) > max(o, a)]
+    slices, bounds = shard_tables(table, G)
 
     # the leaves: G subtree partial sums, each a full-length fp32 vector
     leaf = fc.Plan(table, S, wl.dtype, "tree")
@@ -377,14 +384,14 @@ def shard_share(wl, G, seed=1511, reps=20):
     leaf.close()
     # the owners: one plan per slice over the G partials; every slice stepped once
     w_s, v_s = w0.clone(), v0.clone()
-    owners = [fc.Plan(clip(bounds[r], bounds[r + 1]), G, "f32", "tree") for r in range(G)]
+    owners = [fc.Plan(slices[r], G, "f32", "tree") for r in range(G)]
     for r in range(G):
         owners[r].step(parts, w_s, v_s, wl.lr, wl.mu, wl.wd, wl.batch)
     torch.cuda.synchronize()
     w_t, v_t = w0.clone(), v0.clone()
     owner_us = _mean_call_us(owners[0], "step",
                              lambda: owners[0].step(parts, w_t, v_t, wl.lr, wl.mu, wl.wd, wl.batch), reps)
-    slice_params = sum(n for _, n, _, _ in clip(bounds[0], bounds[1]))
+    slice_params = sum(n for _, n, _, _ in slices[0])
     for p in owners:
         p.close()
     # the whole step on one GPU, for comparison

@@ -1,6 +1,6 @@
 """bench.py's parts that need no GPU: the one-GPU contract, the kernel-source
-hash that ties profiles/ to the sources, and the algorithmic byte counts the
-roofline entry divides by."""
+hash that ties profiles/ to the sources, the algorithmic byte counts the
+roofline entry divides by, and the slicing of --shard."""
 import os
 import subprocess
 import sys
@@ -100,3 +100,36 @@ def test_profile_time_needs_the_current_sources(tmp_path, monkeypatch):
     (prof / "traffic_x.txt").write_text("kernel: step\nkernel_source_sha256_16: 0000000000000000\n"
                                         "rocprof_us_per_step: 12.5\n")
     assert bench.read_profile_us("x", "step") is None
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 8, 64])
+def test_shard_tables_partition_the_segments(G):
+    """The owners' tables of --shard cover every segment element exactly once,
+    keep each element's multipliers, start every slice on a multiple of 64
+    elements, and keep offsets on multiples of 4 (what a plan requires)."""
+    import numpy as np
+
+    import bench
+    from workloads import gen, tables
+
+    rng = np.random.default_rng(G)
+    cases = [tables.get("googlenet").table(), tables.get("nin").table()]
+    for _ in range(5):
+        rows, _ = gen.random_table(rng, int(rng.integers(1, 20)), int(rng.integers(1, 5000)), 4, gap_max=40)
+        cases.append([(o, n, float(rng.integers(1, 4)), float(rng.integers(0, 3))) for o, n, _, _ in rows])
+    for table in cases:
+        slices, bounds = bench.shard_tables(table, G)
+        assert len(slices) == G and bounds[0] == 0 and all(b % 64 == 0 for b in bounds[:-1])
+        ext = max(o + n for o, n, _, _ in table)
+        want = np.full((2, ext), np.nan)
+        for o, n, lr, dm in table:
+            want[:, o:o + n] = [[lr], [dm]]
+        got = np.full((2, ext), np.nan)
+        count = np.zeros(ext, np.int64)
+        for r, sl in enumerate(slices):
+            for o, n, lr, dm in sl:
+                assert o % 4 == 0 and n > 0 and bounds[r] <= o and o + n <= bounds[r + 1]
+                got[:, o:o + n] = [[lr], [dm]]
+                count[o:o + n] += 1
+        assert np.array_equal(count, (~np.isnan(want[0])).astype(np.int64))
+        assert np.array_equal(got, want, equal_nan=True)
