@@ -122,9 +122,9 @@ typedef struct fc_plan fc_plan;
  *   fc_broadcast one launch of grid x rounds blocks.  Same tiles, ranges and
  *   bits as RESIDENT (fc_plan_query reports this value); for a plan of one
  *   round the launches are the same.  With several rounds it is slower on
- *   MI355X (VGG-19 K=16 fp32, 8 rounds: 1785-1790 us per step vs 1771 us
- *   with one launch per round): within one launch the blocks drift apart, so
- *   one round's writes meet the next round's replica reads.
+ *   MI355X (VGG-19 K=16 fp32, 8 rounds: 1802-1805 us per step vs 1763-1764
+ *   us with one launch per round): within one launch the blocks drift apart,
+ *   so one round's writes meet the next round's replica reads.
  * AUTO (no launch-shape field given): FUSED for a step of less than 64 MiB
  *   (n_elems * (K * bytes per element + 16)); otherwise RESIDENT when one
  *   round holds the plan or a parameter's replicas take at least 48 bytes
